@@ -1,0 +1,59 @@
+"""Float64 CPU oracle for the Zarya slot-scoring step.
+
+TEST INFRASTRUCTURE ONLY. Only the test suite, the smoke check and the
+benchmark's CPU-baseline leg may import this package. The product path (the
+HIP library and its Python binding) never imports, calls or links anything
+here, and nothing here imports the product path.
+
+What it computes, each function citing the passage of the paper it follows
+(Sinev, Koziev, Leshchuk, "Zarya: A Hybrid Autoregressive--Masked Diffusion
+Language Model with Flexible Training and Dual-Mode Inference"):
+
+* ``attention``   -- masked softmax attention of S draft slots x L tokens
+  against a reused prefix KV cache (Sec. 5.1 KV-reuse argument, Sec. 5.2
+  draft and verification phases, Sec. 3.1 causal masked reconstruction).
+* ``confidence``  -- full-vocabulary softmax statistics of the LM head
+  (Sec. 5.2 "probability of its first token", Table 1 tied embedding).
+* ``selection``   -- slot confidence and first-hitting slot selection
+  (Sec. 5.2 slot selection, Sec. 6 inference settings).
+
+Every function is the plain definition written out in float64 numpy; there is
+no blocking, fusion or reordering beyond what the definition states.
+"""
+
+from .attention import (
+    PASS_DIFFUSION,
+    PASS_AR_INFILL,
+    CROSS_SLOT_NONE,
+    CROSS_SLOT_CAUSAL,
+    visibility,
+    slot_attention,
+    slot_attention_loops,
+)
+from .confidence import slot_confidence, slot_confidence_loops
+from .selection import (
+    CONF_FIRST_TOKEN,
+    CONF_MEAN,
+    SELECT_THRESHOLD,
+    SELECT_TOP_K,
+    slot_conf,
+    select_slots,
+)
+
+__all__ = [
+    "PASS_DIFFUSION",
+    "PASS_AR_INFILL",
+    "CROSS_SLOT_NONE",
+    "CROSS_SLOT_CAUSAL",
+    "visibility",
+    "slot_attention",
+    "slot_attention_loops",
+    "slot_confidence",
+    "slot_confidence_loops",
+    "CONF_FIRST_TOKEN",
+    "CONF_MEAN",
+    "SELECT_THRESHOLD",
+    "SELECT_TOP_K",
+    "slot_conf",
+    "select_slots",
+]

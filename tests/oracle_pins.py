@@ -1,0 +1,369 @@
+"""Pins of the oracle to facts outside itself.
+
+Each ``check_*`` function takes the function under test (the oracle, or a
+deliberately broken copy of it in the mutation tests) and raises
+AssertionError when the pin does not hold.  The pins are textbook special
+cases computed by library routines (torch's scaled_dot_product_attention on
+the CPU in float64, scipy's logsumexp/softmax, numpy's argmax), closed forms,
+invariants, brute force on tiny inputs, and the paper's selection rule.
+"""
+
+from __future__ import annotations
+
+import json
+import os
+
+import numpy as np
+import scipy.special
+import torch
+import torch.nn.functional as F
+
+import oracle
+from oracle import (
+    CROSS_SLOT_CAUSAL,
+    CROSS_SLOT_NONE,
+    PASS_AR_INFILL,
+    PASS_DIFFUSION,
+)
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+TOL = 1e-11
+
+
+def _inputs(seed, B, Hq, Hkv, D, P, S, L, C=None):
+    rng = np.random.default_rng(seed)
+    C = P if C is None else C
+    T = S * L
+    return dict(
+        q=rng.standard_normal((B, Hq, T, D)),
+        k_cache=rng.standard_normal((B, Hkv, C, D)),
+        v_cache=rng.standard_normal((B, Hkv, C, D)),
+        k_slot=rng.standard_normal((B, Hkv, T, D)),
+        v_slot=rng.standard_normal((B, Hkv, T, D)),
+    )
+
+
+def _sdpa(q, k, v, scale, is_causal=False):
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float64))
+    gqa = q.shape[1] != k.shape[1]
+    return F.scaled_dot_product_attention(t(q), t(k), t(v), scale=scale, is_causal=is_causal, enable_gqa=gqa).numpy()
+
+
+def _close(a, b, tol=TOL, what=""):
+    a, b = np.asarray(a, np.float64), np.asarray(b, np.float64)
+    assert a.shape == b.shape, f"{what}: shape {a.shape} vs {b.shape}"
+    err = np.max(np.abs(a - b)) if a.size else 0.0
+    assert err <= tol, f"{what}: max |diff| {err:.3e} > {tol:.1e}"
+
+
+def _call(attn, x, P, S, L, scale, pass_, cross=CROSS_SLOT_NONE, slot_pass=None):
+    return attn(x["q"], x["k_cache"], x["v_cache"], x["k_slot"], x["v_slot"], P, S, L, scale, pass_,
+                cross_slot=cross, slot_pass=slot_pass)
+
+
+# ---------------------------------------------------------------- attention
+
+
+def check_decode_l1(attn):
+    """L = 1: both passes equal ordinary decode of each token over prefix + itself."""
+    B, Hq, Hkv, D, P, S, L = 2, 4, 2, 8, 7, 5, 1
+    x = _inputs(11, B, Hq, Hkv, D, P, S, L)
+    scale = 0.37
+    outs = []
+    for pass_ in (PASS_DIFFUSION, PASS_AR_INFILL):
+        O, lse = _call(attn, x, P, S, L, scale, pass_)
+        for s in range(S):
+            k = np.concatenate([x["k_cache"][:, :, :P], x["k_slot"][:, :, s : s + 1]], axis=2)
+            v = np.concatenate([x["v_cache"][:, :, :P], x["v_slot"][:, :, s : s + 1]], axis=2)
+            ref = _sdpa(x["q"][:, :, s : s + 1], k, v, scale)
+            _close(O[:, :, s : s + 1], ref, what=f"decode O pass={pass_} slot={s}")
+            kk = np.repeat(k, Hq // Hkv, axis=1)
+            scores = scale * np.einsum("bhd,bhjd->bhj", x["q"][:, :, s], kk)
+            _close(lse[:, :, s], scipy.special.logsumexp(scores, axis=-1), what="decode LSE")
+        outs.append((O, lse))
+    _close(outs[0][0], outs[1][0], what="L=1 passes agree")
+
+
+def check_prefill_s1(attn):
+    """S = 1, AR_INFILL: a chunked causal prefill of L tokens after P cached ones.
+
+    The cache has slack rows beyond P that must be ignored.
+    """
+    B, Hq, Hkv, D, P, S, L = 2, 6, 3, 8, 5, 1, 6
+    x = _inputs(12, B, Hq, Hkv, D, P, S, L, C=P + 3)
+    scale = 0.41
+    O, _ = _call(attn, x, P, S, L, scale, PASS_AR_INFILL)
+    rng = np.random.default_rng(5)
+    q_full = np.concatenate([rng.standard_normal((B, Hq, P, D)), x["q"]], axis=2)
+    k_full = np.concatenate([x["k_cache"][:, :, :P], x["k_slot"]], axis=2)
+    v_full = np.concatenate([x["v_cache"][:, :, :P], x["v_slot"]], axis=2)
+    ref = _sdpa(q_full, k_full, v_full, scale, is_causal=True)[:, :, P:]
+    _close(O, ref, what="S=1 causal prefill")
+
+
+def check_blockdiag_p0(attn):
+    """P = 0, DIFFUSION: every slot is an independent full (unmasked) attention."""
+    B, Hq, Hkv, D, P, S, L = 2, 2, 1, 8, 0, 3, 4
+    x = _inputs(13, B, Hq, Hkv, D, P, S, L)
+    scale = 0.5
+    O, _ = _call(attn, x, P, S, L, scale, PASS_DIFFUSION)
+    for s in range(S):
+        sl = slice(s * L, (s + 1) * L)
+        ref = _sdpa(x["q"][:, :, sl], x["k_slot"][:, :, sl], x["v_slot"][:, :, sl], scale)
+        _close(O[:, :, sl], ref, what=f"block-diagonal slot {s}")
+
+
+def check_cross_causal(attn):
+    """cross_slot = CAUSAL with every slot AR_INFILL is causal attention in physical order."""
+    for P in (0, 3):
+        B, Hq, Hkv, D, S, L = 1, 4, 2, 8, 4, 3
+        x = _inputs(14 + P, B, Hq, Hkv, D, P, S, L)
+        scale = 0.3
+        O, _ = _call(attn, x, P, S, L, scale, PASS_AR_INFILL, cross=CROSS_SLOT_CAUSAL)
+        rng = np.random.default_rng(6)
+        q_full = np.concatenate([rng.standard_normal((B, Hq, P, D)), x["q"]], axis=2)
+        k_full = np.concatenate([x["k_cache"][:, :, :P], x["k_slot"]], axis=2)
+        v_full = np.concatenate([x["v_cache"][:, :, :P], x["v_slot"]], axis=2)
+        ref = _sdpa(q_full, k_full, v_full, scale, is_causal=True)[:, :, P:]
+        _close(O, ref, what=f"cross-slot causal P={P}")
+
+
+def check_slot_permutation(attn):
+    """Permuting whole draft slots (queries and their K/V) permutes the outputs."""
+    B, Hq, Hkv, D, P, S, L = 2, 4, 2, 8, 6, 5, 3
+    x = _inputs(15, B, Hq, Hkv, D, P, S, L)
+    perm = np.array([3, 0, 4, 2, 1])
+    rows = (perm[:, None] * L + np.arange(L)[None, :]).reshape(-1)
+    xp = dict(x)
+    for key in ("q", "k_slot", "v_slot"):
+        xp[key] = x[key][:, :, rows]
+    for pass_ in (PASS_DIFFUSION, PASS_AR_INFILL):
+        O, lse = _call(attn, x, P, S, L, 0.35, pass_)
+        Op, lsep = _call(attn, xp, P, S, L, 0.35, pass_)
+        _close(Op, O[:, :, rows], what=f"slot permutation O pass={pass_}")
+        _close(lsep, lse[:, :, rows], what=f"slot permutation LSE pass={pass_}")
+
+
+def check_token_permutation_diffusion(attn):
+    """DIFFUSION: permuting the tokens inside a slot permutes that slot's outputs."""
+    B, Hq, Hkv, D, P, S, L = 1, 2, 1, 8, 4, 3, 5
+    x = _inputs(16, B, Hq, Hkv, D, P, S, L)
+    rng = np.random.default_rng(3)
+    rows = np.concatenate([s * L + rng.permutation(L) for s in range(S)])
+    xp = dict(x)
+    for key in ("q", "k_slot", "v_slot"):
+        xp[key] = x[key][:, :, rows]
+    O, _ = _call(attn, x, P, S, L, 0.35, PASS_DIFFUSION)
+    Op, _ = _call(attn, xp, P, S, L, 0.35, PASS_DIFFUSION)
+    _close(Op, O[:, :, rows], what="in-slot token permutation")
+
+
+def check_last_token_same(attn):
+    """The last token of every slot sees the same keys in both passes."""
+    B, Hq, Hkv, D, P, S, L = 2, 2, 2, 8, 5, 4, 4
+    x = _inputs(17, B, Hq, Hkv, D, P, S, L)
+    Od, ld = _call(attn, x, P, S, L, 0.3, PASS_DIFFUSION)
+    Oa, la = _call(attn, x, P, S, L, 0.3, PASS_AR_INFILL)
+    last = np.arange(S) * L + L - 1
+    _close(Od[:, :, last], Oa[:, :, last], what="last token O")
+    _close(ld[:, :, last], la[:, :, last], what="last token LSE")
+    assert np.max(np.abs(Od[:, :, 0::L] - Oa[:, :, 0::L])) > 1e-3, "first tokens should differ between passes"
+
+
+def check_constant_v(attn):
+    """Constant values: the output equals that value (probabilities sum to 1)."""
+    B, Hq, Hkv, D, P, S, L = 2, 4, 2, 8, 6, 3, 4
+    x = _inputs(18, B, Hq, Hkv, D, P, S, L)
+    rng = np.random.default_rng(9)
+    c = rng.standard_normal((B, Hkv, 1, D))
+    x["v_cache"] = np.broadcast_to(c, x["v_cache"].shape).copy()
+    x["v_slot"] = np.broadcast_to(c, x["v_slot"].shape).copy()
+    for pass_ in (PASS_DIFFUSION, PASS_AR_INFILL):
+        O, _ = _call(attn, x, P, S, L, 0.8, pass_)
+        ref = np.repeat(c, Hq // Hkv, axis=1)
+        _close(O, np.broadcast_to(ref, O.shape), tol=1e-12, what=f"constant V pass={pass_}")
+
+
+def n_visible(P, S, L, pass_, cross=CROSS_SLOT_NONE):
+    """Number of keys a token (s, r) sees, counted from the paper's rule."""
+    counts = np.empty(S * L, dtype=np.int64)
+    for s in range(S):
+        for r in range(L):
+            own = L if pass_ == PASS_DIFFUSION else r + 1
+            counts[s * L + r] = P + own + (s * L if cross == CROSS_SLOT_CAUSAL else 0)
+    return counts
+
+
+def check_identical_keys(attn):
+    """All keys equal: O is the mean of the visible values, LSE = s0 + ln(#visible)."""
+    B, Hq, Hkv, D, P, S, L = 1, 2, 1, 8, 5, 3, 4
+    for pass_ in (PASS_DIFFUSION, PASS_AR_INFILL):
+        for cross in (CROSS_SLOT_NONE, CROSS_SLOT_CAUSAL):
+            x = _inputs(19, B, Hq, Hkv, D, P, S, L)
+            k0 = x["k_slot"][:, :, :1]
+            x["k_cache"] = np.broadcast_to(k0, x["k_cache"].shape).copy()
+            x["k_slot"] = np.broadcast_to(k0, x["k_slot"].shape).copy()
+            scale = 0.45
+            O, lse = _call(attn, x, P, S, L, scale, pass_, cross=cross)
+            cnt = n_visible(P, S, L, pass_, cross)
+            vals = np.concatenate([x["v_cache"][0, 0, :P], x["v_slot"][0, 0]])
+            for h in range(Hq):
+                s0 = scale * (x["q"][0, h] @ k0[0, 0, 0])
+                _close(lse[0, h], s0 + np.log(cnt), what=f"identical keys LSE pass={pass_} cross={cross}")
+                for t in range(S * L):
+                    s, r = divmod(t, L)
+                    idx = list(range(P))
+                    own = range(s * L, s * L + (L if pass_ == PASS_DIFFUSION else r + 1))
+                    earlier = range(0, s * L) if cross == CROSS_SLOT_CAUSAL else range(0)
+                    idx += [P + j for j in earlier] + [P + j for j in own]
+                    _close(O[0, h, t], vals[idx].mean(axis=0), what="identical keys O")
+
+
+def check_bruteforce(attn):
+    """Agreement with the scalar-loop brute force on tiny random inputs."""
+    cases = [
+        (1, 2, 1, 4, 3, 2, 3, None, CROSS_SLOT_NONE),
+        (2, 4, 2, 4, 0, 3, 2, None, CROSS_SLOT_NONE),
+        (1, 3, 1, 4, 2, 3, 2, [[0, 1, 0]], CROSS_SLOT_NONE),
+        (2, 2, 2, 4, 0, 4, 2, [[1, 0, 1, 0], [0, 0, 1, 1]], CROSS_SLOT_CAUSAL),
+        (1, 2, 1, 4, 3, 2, 2, None, CROSS_SLOT_CAUSAL),
+    ]
+    for i, (B, Hq, Hkv, D, P, S, L, sp, cross) in enumerate(cases):
+        x = _inputs(40 + i, B, Hq, Hkv, D, P, S, L, C=P + 1)
+        for pass_ in (PASS_DIFFUSION, PASS_AR_INFILL):
+            O, lse = _call(attn, x, P, S, L, 0.6, pass_, cross=cross, slot_pass=sp)
+            Ob, lseb = oracle.slot_attention_loops(
+                x["q"], x["k_cache"], x["v_cache"], x["k_slot"], x["v_slot"], P, S, L, 0.6, pass_,
+                cross_slot=cross, slot_pass=sp)
+            _close(O, Ob, tol=1e-12, what=f"brute force O case {i}")
+            _close(lse, lseb, tol=1e-12, what=f"brute force LSE case {i}")
+
+
+ATTENTION_CHECKS = [
+    check_decode_l1,
+    check_prefill_s1,
+    check_blockdiag_p0,
+    check_cross_causal,
+    check_slot_permutation,
+    check_token_permutation_diffusion,
+    check_last_token_same,
+    check_constant_v,
+    check_identical_keys,
+    check_bruteforce,
+]
+
+
+# --------------------------------------------------------------- confidence
+
+
+def check_conf_library(conf):
+    """Random rows against scipy's logsumexp/softmax and numpy's argmax."""
+    rng = np.random.default_rng(21)
+    for V in (512, 500):
+        h = rng.standard_normal((9, 32))
+        w = 0.3 * rng.standard_normal((V, 32))
+        t = rng.integers(0, V, 9)
+        r = conf(h, w, target_ids=t)
+        logits = h @ w.T
+        sm = scipy.special.softmax(logits, axis=1)
+        _close(r["lse"], scipy.special.logsumexp(logits, axis=1), what="lse vs scipy")
+        _close(r["max_prob"], sm.max(axis=1), what="max_prob vs softmax")
+        _close(r["target_prob"], sm[np.arange(9), t], what="target_prob vs softmax")
+        assert np.array_equal(r["argmax"], np.argmax(logits, axis=1)), "argmax vs numpy"
+
+
+def check_conf_bruteforce(conf):
+    """Agreement with scalar loops and exactly rounded sums (V = 512 and 500)."""
+    rng = np.random.default_rng(22)
+    for V in (512, 500):
+        h = rng.standard_normal((4, 16))
+        w = 0.5 * rng.standard_normal((V, 16))
+        t = rng.integers(0, V, 4)
+        r = conf(h, w, target_ids=t)
+        b = oracle.slot_confidence_loops(h, w, target_ids=t)
+        for key in ("max_prob", "lse", "target_prob"):
+            _close(r[key], b[key], tol=1e-12, what=f"brute force {key}")
+        assert np.array_equal(r["argmax"], b["argmax"])
+
+
+def check_conf_zero_hidden(conf):
+    """h = 0: every logit is 0, so lse = ln V, max_prob = 1/V, argmax = 0."""
+    V = 777
+    w = np.random.default_rng(23).standard_normal((V, 24))
+    r = conf(np.zeros((3, 24)), w)
+    _close(r["lse"], np.full(3, np.log(V)), what="zero h lse")
+    _close(r["max_prob"], np.full(3, 1.0 / V), what="zero h max_prob")
+    assert np.all(r["argmax"] == 0)
+
+
+def check_conf_planted(conf):
+    """h = a * W[v]/|W[v]| makes v the argmax; max_prob rises towards 1 with a."""
+    rng = np.random.default_rng(24)
+    V, H = 300, 64
+    w = 0.02 * rng.standard_normal((V, H))
+    v_star = 137
+    u = w[v_star] / np.linalg.norm(w[v_star])
+    alphas = np.array([5.0, 15.0, 25.0, 35.0, 60.0])
+    r = conf(alphas[:, None] * u[None, :], w)
+    assert np.all(r["argmax"] == v_star), r["argmax"]
+    assert np.all(np.diff(r["max_prob"]) > 0), r["max_prob"]
+    assert r["max_prob"][-1] > 0.95 and r["max_prob"][0] < 0.05
+
+
+def check_conf_sums_to_one(conf):
+    """Summing the target probability over every vocabulary id gives 1."""
+    rng = np.random.default_rng(25)
+    V, H = 257, 16
+    w = rng.standard_normal((V, H))
+    h = np.repeat(rng.standard_normal((1, H)), V, axis=0)
+    r = conf(h, w, target_ids=np.arange(V))
+    _close(r["target_prob"].sum(), 1.0, tol=1e-12, what="softmax sums to 1")
+    _close(r["max_prob"][0], r["target_prob"].max(), what="max_prob is the largest probability")
+    assert r["argmax"][0] == int(np.argmax(r["target_prob"]))
+
+
+def check_conf_ties(conf):
+    """Equal maximal logits: the lowest vocabulary id wins and the top-2 gap is 0."""
+    rng = np.random.default_rng(26)
+    V, H = 64, 8
+    w = rng.standard_normal((V, H))
+    h = rng.standard_normal((1, H))
+    best = int(np.argmax(h @ w.T))
+    w2 = w.copy()
+    lo = max(0, best - 5)
+    w2[lo] = w[best]
+    r = conf(h, w2)
+    assert r["argmax"][0] == min(lo, best)
+    assert r["top2_gap"][0] == 0.0
+
+
+CONFIDENCE_CHECKS = [
+    check_conf_library,
+    check_conf_bruteforce,
+    check_conf_zero_hidden,
+    check_conf_planted,
+    check_conf_sums_to_one,
+    check_conf_ties,
+]
+
+
+# ---------------------------------------------------------------- selection
+
+
+def load_selection_golden():
+    with open(os.path.join(GOLDEN, "select_slots_cases.json")) as f:
+        return json.load(f)["cases"]
+
+
+def check_select_golden(select):
+    """Hand cases of the paper's selection rule (Sec. 5.2, tau from Sec. 6)."""
+    for case in load_selection_golden():
+        tc = np.array(case["token_conf"], dtype=np.float32)[None]
+        is_open = None if case.get("open") is None else np.array(case["open"], dtype=np.uint8)[None]
+        _, sel, n = select(tc, is_open, case["conf_rule"], case["rule"], case.get("threshold", 0.9), case.get("k", 1))
+        got = [int(s) for s in sel[0, : n[0]]]
+        assert got == case["expect"], f"{case['name']}: got {got}, expected {case['expect']}"
+        assert np.all(sel[0, n[0]:] == -1), f"{case['name']}: padding"
+
+
+SELECTION_CHECKS = [check_select_golden]

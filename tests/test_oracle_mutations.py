@@ -1,0 +1,223 @@
+"""Plant plausible mistakes in copies of the oracle (CPU only) and show the pins catch each.
+
+A pin set that a dropped term, a wrong sign or index, or a transposed operand
+survives would not pin anything; every mutant below must fail at least one
+check of the set that covers its function.
+"""
+
+import numpy as np
+import pytest
+
+import oracle
+import oracle.attention as oatt
+import oracle_pins as pins
+
+
+_ORIG_VIS = oatt.visibility
+
+
+def _with_visibility(bad_visibility):
+    """An attention oracle whose mask comes from ``bad_visibility``."""
+
+    def attn(*args, **kw):
+        saved = oatt.visibility
+        oatt.visibility = bad_visibility
+        try:
+            return oracle.slot_attention(*args, **kw)
+        finally:
+            oatt.visibility = saved
+
+    return attn
+
+
+def _vis_flipped_causal(P, S, L, pass_, cross_slot=0, slot_pass=None):
+    m = _ORIG_VIS(P, S, L, pass_, cross_slot, slot_pass)
+    for s in range(S):
+        rows = slice(s * L, (s + 1) * L)
+        own = slice(P + s * L, P + (s + 1) * L)
+        sp = pass_ if slot_pass is None else slot_pass[s]
+        if sp == oracle.PASS_AR_INFILL:
+            m[rows, own] = np.triu(np.ones((L, L), bool))  # looks forward instead of back
+    return m
+
+
+def _vis_diffusion_as_causal(P, S, L, pass_, cross_slot=0, slot_pass=None):
+    return _ORIG_VIS(P, S, L, oracle.PASS_AR_INFILL, cross_slot, None)
+
+
+def _vis_no_prefix(P, S, L, pass_, cross_slot=0, slot_pass=None):
+    m = _ORIG_VIS(P, S, L, pass_, cross_slot, slot_pass)
+    m[:, :P] = False
+    return m
+
+
+def _vis_slots_leak(P, S, L, pass_, cross_slot=0, slot_pass=None):
+    m = _ORIG_VIS(P, S, L, pass_, cross_slot, slot_pass)
+    m[:, P:] = True  # every slot sees every other slot
+    return m
+
+
+def _vis_boundary_off_by_one(P, S, L, pass_, cross_slot=0, slot_pass=None):
+    m = _ORIG_VIS(P, S, L, pass_, cross_slot, slot_pass)
+    return np.roll(m, 1, axis=1) | np.eye(S * L, P + S * L, k=P, dtype=bool)
+
+
+def _vis_excludes_diagonal(P, S, L, pass_, cross_slot=0, slot_pass=None):
+    m = _ORIG_VIS(P, S, L, pass_, cross_slot, slot_pass)
+    if P > 0:
+        idx = np.arange(S * L)
+        m[idx, P + idx] = False
+    return m
+
+
+def _attn_no_scale(q, kc, vc, ks, vs, P, S, L, scale, pass_, **kw):
+    return oracle.slot_attention(q, kc, vc, ks, vs, P, S, L, 1.0, pass_, **kw)
+
+
+def _attn_gqa_modulo(q, kc, vc, ks, vs, P, S, L, scale, pass_, **kw):
+    # query head h reads KV head h % Hkv instead of h // G
+    Hq, Hkv = q.shape[1], ks.shape[1]
+    perm = sorted(range(Hq), key=lambda h: (h % Hkv, h))
+    O, lse = oracle.slot_attention(q[:, perm], kc, vc, ks, vs, P, S, L, scale, pass_, **kw)
+    Om, lsem = np.empty_like(O), np.empty_like(lse)
+    Om[:, perm], lsem[:, perm] = O, lse
+    return Om, lsem
+
+
+def _attn_lse_without_max(q, kc, vc, ks, vs, P, S, L, scale, pass_, **kw):
+    O, lse = oracle.slot_attention(q, kc, vc, ks, vs, P, S, L, scale, pass_, **kw)
+    s = scale * np.einsum("bhtd,bhtd->bht", q, np.repeat(ks, q.shape[1] // ks.shape[1], axis=1))
+    return O, lse - np.maximum(s, 0)  # forgot part of the max shift
+
+
+def _attn_values_from_keys(q, kc, vc, ks, vs, P, S, L, scale, pass_, **kw):
+    return oracle.slot_attention(q, kc, kc, ks, ks, P, S, L, scale, pass_, **kw)
+
+
+ATTENTION_MUTANTS = {
+    "no softmax scale": _attn_no_scale,
+    "AR_INFILL looks forward": _with_visibility(_vis_flipped_causal),
+    "DIFFUSION treated as causal": _with_visibility(_vis_diffusion_as_causal),
+    "prefix dropped": _with_visibility(_vis_no_prefix),
+    "slots see each other": _with_visibility(_vis_slots_leak),
+    "slot boundary off by one": _with_visibility(_vis_boundary_off_by_one),
+    "token does not see itself": _with_visibility(_vis_excludes_diagonal),
+    "GQA head mapping h % Hkv": _attn_gqa_modulo,
+    "LSE missing the max shift": _attn_lse_without_max,
+    "values taken from keys": _attn_values_from_keys,
+}
+
+
+def _conf_wrong_tie(h, w, target_ids=None, row_chunk=256):
+    r = oracle.slot_confidence(h, w, target_ids, row_chunk)
+    logits = np.asarray(h, np.float64) @ np.asarray(w, np.float64).T
+    r["argmax"] = logits.shape[1] - 1 - np.argmax(logits[:, ::-1], axis=1)  # highest id on ties
+    return r
+
+
+def _conf_lse_missing_max(h, w, target_ids=None, row_chunk=256):
+    r = oracle.slot_confidence(h, w, target_ids, row_chunk)
+    r["lse"] = r["lse"] - r["max_logit"]
+    return r
+
+
+def _conf_shuffled_vocab(h, w, target_ids=None, row_chunk=256):
+    w = np.asarray(w)
+    perm = np.roll(np.arange(w.shape[0]), 1)
+    return oracle.slot_confidence(h, w[perm], target_ids, row_chunk)
+
+
+def _conf_target_is_argmax(h, w, target_ids=None, row_chunk=256):
+    r = oracle.slot_confidence(h, w, target_ids, row_chunk)
+    if target_ids is not None:
+        r["target_prob"] = r["max_prob"].copy()
+    return r
+
+
+def _conf_prob_without_normaliser(h, w, target_ids=None, row_chunk=256):
+    r = oracle.slot_confidence(h, w, target_ids, row_chunk)
+    r["max_prob"] = 1.0 / (1.0 + np.exp(-r["max_logit"]))
+    return r
+
+
+CONFIDENCE_MUTANTS = {
+    "argmax takes the highest id on ties": _conf_wrong_tie,
+    "lse without the max": _conf_lse_missing_max,
+    "vocab rows shifted by one": _conf_shuffled_vocab,
+    "target prob is the max prob": _conf_target_is_argmax,
+    "sigmoid instead of softmax": _conf_prob_without_normaliser,
+}
+
+
+def _sel_non_strict(tc, op=None, cr=0, rule=0, threshold=0.9, k=1):
+    return oracle.select_slots(tc, op, cr, rule, np.nextafter(np.float32(threshold), np.float32(0)), k)
+
+
+def _sel_fallback_highest_index(tc, op=None, cr=0, rule=0, threshold=0.9, k=1):
+    c, sel, n = oracle.select_slots(tc, op, cr, rule, threshold, k)
+    conf = oracle.slot_conf(tc, cr)
+    for b in range(sel.shape[0]):
+        if n[b] == 1 and not conf[b, sel[b, 0]] > np.float32(threshold) and rule == 0:
+            is_open = np.ones(conf.shape[1], bool) if op is None else op[b] != 0
+            cand = [s for s in range(conf.shape[1]) if is_open[s] and conf[b, s] == conf[b, sel[b, 0]]]
+            sel[b, 0] = max(cand)
+    return c, sel, n
+
+
+def _sel_slot_order(tc, op=None, cr=0, rule=0, threshold=0.9, k=1):
+    c, sel, n = oracle.select_slots(tc, op, cr, rule, threshold, k)
+    for b in range(sel.shape[0]):
+        sel[b, : n[b]] = np.sort(sel[b, : n[b]])
+    return c, sel, n
+
+
+def _sel_mean_is_first(tc, op=None, cr=0, rule=0, threshold=0.9, k=1):
+    return oracle.select_slots(tc, op, oracle.CONF_FIRST_TOKEN, rule, threshold, k)
+
+
+def _sel_ignores_open(tc, op=None, cr=0, rule=0, threshold=0.9, k=1):
+    return oracle.select_slots(tc, None, cr, rule, threshold, k)
+
+
+def _sel_no_fallback(tc, op=None, cr=0, rule=0, threshold=0.9, k=1):
+    c, sel, n = oracle.select_slots(tc, op, cr, rule, threshold, k)
+    conf = oracle.slot_conf(tc, cr)
+    for b in range(sel.shape[0]):
+        if rule == 0 and n[b] == 1 and not conf[b, sel[b, 0]] > np.float32(threshold):
+            sel[b, 0], n[b] = -1, 0
+    return c, sel, n
+
+
+SELECTION_MUTANTS = {
+    "threshold compared with >=": _sel_non_strict,
+    "fallback takes the highest index on ties": _sel_fallback_highest_index,
+    "output in slot order": _sel_slot_order,
+    "mean rule uses the first token": _sel_mean_is_first,
+    "closed slots ignored": _sel_ignores_open,
+    "no fallback": _sel_no_fallback,
+}
+
+
+def _caught(fn, checks):
+    failed = []
+    for check in checks:
+        try:
+            check(fn)
+        except (AssertionError, ValueError, IndexError) as e:  # noqa: PERF203
+            failed.append((check.__name__, str(e)[:80]))
+    return failed
+
+
+@pytest.mark.parametrize("name", list(ATTENTION_MUTANTS))
+def test_attention_mutant_is_caught(name):
+    assert _caught(ATTENTION_MUTANTS[name], pins.ATTENTION_CHECKS), f"mutant '{name}' passed every pin"
+
+
+@pytest.mark.parametrize("name", list(CONFIDENCE_MUTANTS))
+def test_confidence_mutant_is_caught(name):
+    assert _caught(CONFIDENCE_MUTANTS[name], pins.CONFIDENCE_CHECKS), f"mutant '{name}' passed every pin"
+
+
+@pytest.mark.parametrize("name", list(SELECTION_MUTANTS))
+def test_selection_mutant_is_caught(name):
+    assert _caught(SELECTION_MUTANTS[name], pins.SELECTION_CHECKS), f"mutant '{name}' passed every pin"
