@@ -1,0 +1,216 @@
+/*
+ * zarya.h -- C ABI of the Zarya slot-scoring step on AMD Instinct MI355X (gfx950).
+ *
+ * One scoring step of slotted speculative decoding (paper: Zarya, Sec. 5.2,
+ * "Mode B: Slotted Speculative Decoding") is
+ *
+ *   1. zarya_slot_attn        attention of S draft slots x L tokens against the
+ *                             reused prefix KV cache (Sec. 5.1 KV-reuse argument,
+ *                             Sec. 5.2 draft and verification phases);
+ *   2. zarya_slot_confidence  LM-head projection reduced on the fly to per-token
+ *                             softmax statistics (Sec. 5.2 "probability of its
+ *                             first token"; Table 1 tied embedding);
+ *   3. zarya_select_slots     slot confidence and first-hitting slot selection
+ *                             (Sec. 5.2 "Slot selection"; Sec. 6 threshold 0.9).
+ *
+ * Conventions for every entry point:
+ *  - Tensor arguments are DEVICE pointers to dense row-major (C-contiguous)
+ *    arrays whose shapes are given in the comments; the caller owns every
+ *    buffer, including the workspace.  The library never allocates or frees
+ *    device memory and keeps no state between calls.
+ *  - Calls only enqueue work on `stream` (0 = the null stream); nothing waits
+ *    for the GPU.  Results are ready when the stream is.
+ *  - Arguments are validated on the host before anything is launched.  A
+ *    non-OK status means nothing was enqueued, except ZARYA_ERR_HIP, which
+ *    reports a failed launch.  zarya_last_error() returns a message for the
+ *    last non-OK status returned on the calling thread.
+ *  - Results are bit-identical from run to run for the same arguments (no
+ *    floating-point atomics; every reduction has a fixed order).
+ *  - Entry points are reentrant.  Calls that share an output or workspace
+ *    buffer must be ordered by the caller (same stream or events).
+ */
+#ifndef ZARYA_H
+#define ZARYA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ZARYA_VERSION_MAJOR 0
+#define ZARYA_VERSION_MINOR 1
+
+typedef enum zarya_status {
+  ZARYA_OK = 0,
+  ZARYA_ERR_INVALID_ARGUMENT = 1,    /* NULL pointer, bad size, inconsistent shape      */
+  ZARYA_ERR_UNSUPPORTED = 2,         /* valid request this build does not implement     */
+  ZARYA_ERR_WORKSPACE_TOO_SMALL = 3, /* workspace_bytes below the *_workspace_size value */
+  ZARYA_ERR_HIP = 4                  /* a HIP launch or runtime call failed              */
+} zarya_status;
+
+typedef enum zarya_dtype {
+  ZARYA_DTYPE_F32 = 0,  /* IEEE float32 storage and arithmetic                    */
+  ZARYA_DTYPE_BF16 = 1  /* bfloat16 storage, float32 accumulation (Sec. 6: BF16) */
+} zarya_dtype;
+
+/* In-slot attention pattern of a pass (Sec. 5.2). */
+typedef enum zarya_pass {
+  ZARYA_PASS_DIFFUSION = 0, /* draft phase: a token sees every token of its own slot   */
+  ZARYA_PASS_AR_INFILL = 1  /* verification phase: a token sees its own slot up to itself */
+} zarya_pass;
+
+/* Whether a draft slot sees earlier slots (Sec. 3.1 causal layout). */
+typedef enum zarya_cross_slot {
+  ZARYA_CROSS_SLOT_NONE = 0,  /* scoring path: prefix + own slot only (slots are parallel) */
+  ZARYA_CROSS_SLOT_CAUSAL = 1 /* every earlier slot is visible too (reordered training layout) */
+} zarya_cross_slot;
+
+/* ------------------------------------------------------------------------ */
+/* 1. Slot-parallel attention against the prefix KV cache                    */
+/* ------------------------------------------------------------------------ */
+/*
+ * Physical order of one sequence (Sec. 5.2 "Reordering": masked tokens follow
+ * the unmasked ones): the P committed prefix tokens, whose K/V live in the
+ * cache, then the draft slots 0..S-1 of L tokens each (T = S*L tokens), whose
+ * own K/V are passed separately.  Draft token t = s*L + r (slot s, position r)
+ * of query head h (KV head g = h / (Hq/Hkv)) attends to
+ *   - every prefix key j < P (the cache is read-only; Sec. 5.1 KV reuse),
+ *   - the keys of its own slot: all L of them in the DIFFUSION pass, those at
+ *     positions r' <= r in the AR_INFILL pass,
+ *   - with cross_slot = CAUSAL, also every key of slots s' < s.
+ * Softmax scale `softmax_scale` is applied to q.k before the softmax.
+ *
+ * Output O[b,h,t,:] = sum_j p_j v_j with p the masked softmax, and
+ * lse[b,h,t] = ln(sum_j exp(scale * q.k_j)) over the visible keys (natural log).
+ */
+typedef struct zarya_slot_attn_desc {
+  int32_t batch;         /* B >= 1                                              */
+  int32_t n_q_heads;     /* Hq >= 1                                             */
+  int32_t n_kv_heads;    /* Hkv >= 1, Hq % Hkv == 0                             */
+  int32_t head_dim;      /* D: 64 or 128                                        */
+  int32_t prefix_len;    /* P >= 0 valid cache rows                             */
+  int32_t kv_capacity;   /* C >= P: row count (token stride) of the cache arrays */
+  int32_t n_slots;       /* S >= 1                                              */
+  int32_t slot_len;      /* L >= 1                                              */
+  float softmax_scale;   /* finite, > 0 (1/sqrt(D) in the usual model)          */
+  int32_t pass;          /* zarya_pass, used for slots without a slot_pass entry */
+  int32_t cross_slot;    /* zarya_cross_slot                                    */
+  int32_t dtype;         /* zarya_dtype of q, caches, slot K/V and out          */
+  int32_t prefix_splits; /* 0 = library's choice; 1..64 = split the prefix keys
+                            into at most this many ranges processed by
+                            separate workgroups and merged exactly (results
+                            agree to float32 rounding for every choice; the
+                            F32 path ignores it)                             */
+} zarya_slot_attn_desc;
+
+/* Bytes of device workspace zarya_slot_attn needs for `desc` (may be 0). */
+zarya_status zarya_slot_attn_workspace_size(const zarya_slot_attn_desc* desc, size_t* bytes);
+
+/*
+ * q         [B, Hq, T, D]  dtype   draft-token queries, T = S*L, row t = s*L + r
+ * k_cache   [B, Hkv, C, D] dtype   prefix keys; rows >= P are never read;
+ * v_cache   [B, Hkv, C, D] dtype   may be NULL only when P == 0
+ * k_slot    [B, Hkv, T, D] dtype   the draft tokens' own keys
+ * v_slot    [B, Hkv, T, D] dtype   the draft tokens' own values
+ * slot_pass [B, S] uint8 or NULL   per-slot zarya_pass overriding desc->pass
+ * out       [B, Hq, T, D]  dtype   attention output (bf16: round to nearest even)
+ * lse       [B, Hq, T] float32 or NULL
+ * workspace device buffer of at least zarya_slot_attn_workspace_size bytes
+ *           (may be NULL when that size is 0); contents on entry do not matter
+ *
+ * slot_pass entries: 0 = DIFFUSION, any other value = AR_INFILL.
+ *
+ * ZARYA_ERR_UNSUPPORTED: head_dim not 64 or 128; B*Hq*T or B*Hkv*C at or above 2^31.
+ */
+zarya_status zarya_slot_attn(const zarya_slot_attn_desc* desc, const void* q, const void* k_cache,
+                             const void* v_cache, const void* k_slot, const void* v_slot,
+                             const uint8_t* slot_pass, void* out, float* lse, void* workspace,
+                             size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* 2. LM-head confidence: logits = hidden . W^T reduced per row on the fly   */
+/* ------------------------------------------------------------------------ */
+/*
+ * For every row i of `hidden` (rows ordered (b, s, r)) with logits
+ * z_v = hidden[i,:] . w_vocab[v,:] over the whole vocabulary v < V:
+ *   argmax_id[i]   = the smallest v with z_v = max_v z_v
+ *   lse[i]         = ln sum_v exp(z_v)
+ *   max_prob[i]    = exp(max_v z_v - lse[i])   (largest softmax probability)
+ *   target_prob[i] = exp(z_{target_ids[i]} - lse[i])
+ * Logits are computed in float32 and never written to memory.
+ */
+typedef struct zarya_conf_desc {
+  int32_t n_rows; /* M >= 1                                              */
+  int32_t hidden; /* H >= 1; a multiple of 8 for BF16                    */
+  int32_t vocab;  /* V >= 1                                              */
+  int32_t dtype;  /* zarya_dtype of hidden and w_vocab                   */
+} zarya_conf_desc;
+
+zarya_status zarya_slot_confidence_workspace_size(const zarya_conf_desc* desc, size_t* bytes);
+
+/*
+ * hidden      [M, H] dtype      final hidden states of the draft tokens
+ * w_vocab     [V, H] dtype      LM-head weight = tied token embedding (Table 1)
+ * target_ids  [M] int32 or NULL ids in [0, V) (checked on the GPU: an id out of
+ *                               range gives target_prob = NaN); NULL skips target_prob
+ * max_prob    [M] float32       required
+ * argmax_id   [M] int32         required
+ * lse         [M] float32 or NULL
+ * target_prob [M] float32 or NULL (ignored when target_ids is NULL)
+ * workspace   at least zarya_slot_confidence_workspace_size bytes
+ */
+zarya_status zarya_slot_confidence(const zarya_conf_desc* desc, const void* hidden, const void* w_vocab,
+                                   const int32_t* target_ids, float* max_prob, int32_t* argmax_id,
+                                   float* lse, float* target_prob, void* workspace,
+                                   size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* 3. First-hitting slot selection                                           */
+/* ------------------------------------------------------------------------ */
+typedef enum zarya_slot_conf_rule {
+  ZARYA_SLOT_CONF_FIRST_TOKEN = 0, /* confidence of the slot's first token (Sec. 5.2) */
+  ZARYA_SLOT_CONF_MEAN = 1         /* mean over the slot's L tokens: summed in float64
+                                      in token order, divided by L, rounded once to float32 */
+} zarya_slot_conf_rule;
+
+typedef enum zarya_select_rule {
+  ZARYA_SELECT_THRESHOLD = 0, /* every open slot with confidence > threshold (strict);
+                                 if none, the single most confident open slot (Sec. 5.2) */
+  ZARYA_SELECT_TOP_K = 1      /* the k most confident open slots                      */
+} zarya_select_rule;
+
+/*
+ * token_conf  [B, S, L] float32   per-token confidence (max_prob of slot_confidence)
+ * slot_open   [B, S] uint8 or NULL  nonzero = slot still undecided; NULL = all open
+ * slot_conf   [B, S] float32 out  slot confidence; -1 for closed slots
+ * selected    [B, S] int32 out    chosen slot ids in first-hitting order (descending
+ *                                 confidence, ties to the lower slot index), then -1
+ * n_selected  [B] int32 out       number of chosen slots
+ * Comparisons are made between float32 values; `threshold` is used as given.
+ * Requires 1 <= S <= 1024 and k >= 0 for TOP_K.
+ */
+zarya_status zarya_select_slots(int32_t batch, int32_t n_slots, int32_t slot_len, const float* token_conf,
+                                const uint8_t* slot_open, int32_t conf_rule, int32_t rule, float threshold,
+                                int32_t k, float* slot_conf, int32_t* selected, int32_t* n_selected,
+                                hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Diagnostics                                                               */
+/* ------------------------------------------------------------------------ */
+/* Static name of a status code; never NULL. */
+const char* zarya_status_string(zarya_status status);
+/* Message for the last non-OK status returned on this thread ("" if none).
+   The pointer stays valid until the next zarya_* call on the same thread. */
+const char* zarya_last_error(void);
+/* ZARYA_VERSION_MAJOR * 1000 + ZARYA_VERSION_MINOR of the built library. */
+int32_t zarya_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ZARYA_H */

@@ -1,0 +1,180 @@
+"""Zarya slot-scoring step on MI355X: Python binding of libzarya (HIP, gfx950).
+
+The three calls of one scoring step of slotted speculative decoding
+(Zarya, Sec. 5.2):
+
+* :func:`slot_attn`        -- slot-parallel attention against the prefix cache
+* :func:`slot_confidence`  -- LM-head softmax statistics, logits kept on chip
+* :func:`select_slots`     -- first-hitting slot selection
+
+Each function marshals torch tensors (device memory) and torch's current
+stream into the C ABI of ``include/zarya.h``; all arithmetic runs in the HIP
+kernels.  Outputs and workspaces are allocated with torch unless passed in.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import math
+
+import torch
+
+from . import _lib
+from ._lib import (  # noqa: F401
+    CROSS_SLOT_CAUSAL,
+    CROSS_SLOT_NONE,
+    DTYPE_BF16,
+    DTYPE_F32,
+    PASS_AR_INFILL,
+    PASS_DIFFUSION,
+    SELECT_THRESHOLD,
+    SELECT_TOP_K,
+    SLOT_CONF_FIRST_TOKEN,
+    SLOT_CONF_MEAN,
+    ZaryaError,
+)
+
+__all__ = [
+    "slot_attn",
+    "slot_attn_desc",
+    "slot_confidence",
+    "select_slots",
+    "ZaryaError",
+    "PASS_DIFFUSION",
+    "PASS_AR_INFILL",
+    "CROSS_SLOT_NONE",
+    "CROSS_SLOT_CAUSAL",
+    "SLOT_CONF_FIRST_TOKEN",
+    "SLOT_CONF_MEAN",
+    "SELECT_THRESHOLD",
+    "SELECT_TOP_K",
+]
+
+_DT = {torch.bfloat16: DTYPE_BF16, torch.float32: DTYPE_F32}
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _need(t, name, shape, dtype, device):
+    if t.device != device or t.dtype != dtype or tuple(t.shape) != tuple(shape) or not t.is_contiguous():
+        raise ValueError(
+            f"{name}: expected contiguous {dtype} {tuple(shape)} on {device}, "
+            f"got {t.dtype} {tuple(t.shape)} on {t.device} (contiguous={t.is_contiguous()})"
+        )
+
+
+def slot_attn_desc(q, k_cache, k_slot, n_slots, slot_len, pass_=PASS_DIFFUSION, cross_slot=CROSS_SLOT_NONE,
+                   prefix_len=None, softmax_scale=None, prefix_splits=0):
+    B, Hq, T, D = q.shape
+    Hkv = k_slot.shape[1]
+    C = 0 if k_cache is None else k_cache.shape[2]
+    P = C if prefix_len is None else int(prefix_len)
+    if q.dtype not in _DT:
+        raise ValueError(f"unsupported dtype {q.dtype}")
+    return _lib.SlotAttnDesc(
+        batch=B, n_q_heads=Hq, n_kv_heads=Hkv, head_dim=D, prefix_len=P, kv_capacity=C,
+        n_slots=int(n_slots), slot_len=int(slot_len),
+        softmax_scale=float(1.0 / math.sqrt(D) if softmax_scale is None else softmax_scale),
+        pass_=int(pass_), cross_slot=int(cross_slot), dtype=_DT[q.dtype], prefix_splits=int(prefix_splits),
+    )
+
+
+def slot_attn(q, k_cache, v_cache, k_slot, v_slot, n_slots, slot_len, pass_=PASS_DIFFUSION,
+              cross_slot=CROSS_SLOT_NONE, slot_pass=None, prefix_len=None, softmax_scale=None,
+              out=None, lse=None, want_lse=True, workspace=None, prefix_splits=0):
+    """Attention of S draft slots x L tokens against a prefix KV cache.
+
+    q [B,Hq,T,D], k_cache/v_cache [B,Hkv,C,D] (or None when there is no
+    prefix), k_slot/v_slot [B,Hkv,T,D], slot_pass [B,S] uint8 or None.
+    Returns (out [B,Hq,T,D], lse [B,Hq,T] float32 or None).
+    """
+    B, Hq, T, D = q.shape
+    dev, dt = q.device, q.dtype
+    Hkv = k_slot.shape[1]
+    desc = slot_attn_desc(q, k_cache, k_slot, n_slots, slot_len, pass_, cross_slot, prefix_len, softmax_scale,
+                          prefix_splits)
+    _need(q, "q", (B, Hq, T, D), dt, dev)
+    _need(k_slot, "k_slot", (B, Hkv, T, D), dt, dev)
+    _need(v_slot, "v_slot", (B, Hkv, T, D), dt, dev)
+    if k_cache is not None:
+        _need(k_cache, "k_cache", (B, Hkv, desc.kv_capacity, D), dt, dev)
+        _need(v_cache, "v_cache", (B, Hkv, desc.kv_capacity, D), dt, dev)
+    if slot_pass is not None:
+        _need(slot_pass, "slot_pass", (B, n_slots), torch.uint8, dev)
+    if out is None:
+        out = torch.empty((B, Hq, T, D), dtype=dt, device=dev)
+    _need(out, "out", (B, Hq, T, D), dt, dev)
+    if lse is None and want_lse:
+        lse = torch.empty((B, Hq, T), dtype=torch.float32, device=dev)
+    if lse is not None:
+        _need(lse, "lse", (B, Hq, T), torch.float32, dev)
+    ws_bytes = _lib.slot_attn_workspace_size(desc)
+    if workspace is None and ws_bytes > 0:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    _lib.check(_lib.lib().zarya_slot_attn(
+        ctypes.byref(desc), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(k_slot), _ptr(v_slot), _ptr(slot_pass),
+        _ptr(out), _ptr(lse), _ptr(workspace), 0 if workspace is None else workspace.numel(), _stream()))
+    return out, lse
+
+
+def slot_confidence(hidden, w_vocab, target_ids=None, out=None, workspace=None):
+    """Per-row softmax statistics of hidden . w_vocab^T over the full vocabulary.
+
+    hidden [M,H], w_vocab [V,H] (bf16 or float32), target_ids [M] int32 or None.
+    Returns a dict with ``max_prob``, ``argmax``, ``lse`` (float32/int32 [M])
+    and ``target_prob`` when target ids are given.
+    """
+    M, H = hidden.shape
+    V = w_vocab.shape[0]
+    dev, dt = hidden.device, hidden.dtype
+    _need(hidden, "hidden", (M, H), dt, dev)
+    _need(w_vocab, "w_vocab", (V, H), dt, dev)
+    if target_ids is not None:
+        _need(target_ids, "target_ids", (M,), torch.int32, dev)
+    desc = _lib.ConfDesc(n_rows=M, hidden=H, vocab=V, dtype=_DT[dt])
+    if out is None:
+        out = {
+            "max_prob": torch.empty(M, dtype=torch.float32, device=dev),
+            "argmax": torch.empty(M, dtype=torch.int32, device=dev),
+            "lse": torch.empty(M, dtype=torch.float32, device=dev),
+        }
+        if target_ids is not None:
+            out["target_prob"] = torch.empty(M, dtype=torch.float32, device=dev)
+    ws_bytes = _lib.slot_confidence_workspace_size(desc)
+    if workspace is None:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    _lib.check(_lib.lib().zarya_slot_confidence(
+        ctypes.byref(desc), _ptr(hidden), _ptr(w_vocab), _ptr(target_ids), _ptr(out["max_prob"]),
+        _ptr(out["argmax"]), _ptr(out.get("lse")), _ptr(out.get("target_prob")), _ptr(workspace),
+        workspace.numel(), _stream()))
+    return out
+
+
+def select_slots(token_conf, slot_open=None, conf_rule=SLOT_CONF_FIRST_TOKEN, rule=SELECT_THRESHOLD,
+                 threshold=0.9, k=1, out=None):
+    """First-hitting slot selection from per-token confidences [B,S,L] float32.
+
+    Returns (slot_conf [B,S] float32, selected [B,S] int32, n_selected [B] int32).
+    """
+    B, S, L = token_conf.shape
+    dev = token_conf.device
+    _need(token_conf, "token_conf", (B, S, L), torch.float32, dev)
+    if slot_open is not None:
+        _need(slot_open, "slot_open", (B, S), torch.uint8, dev)
+    if out is None:
+        out = (
+            torch.empty((B, S), dtype=torch.float32, device=dev),
+            torch.empty((B, S), dtype=torch.int32, device=dev),
+            torch.empty((B,), dtype=torch.int32, device=dev),
+        )
+    slot_conf, selected, n_selected = out
+    _lib.check(_lib.lib().zarya_select_slots(
+        B, S, L, _ptr(token_conf), _ptr(slot_open), int(conf_rule), int(rule), float(threshold), int(k),
+        _ptr(slot_conf), _ptr(selected), _ptr(n_selected), _stream()))
+    return slot_conf, selected, n_selected

@@ -1,0 +1,132 @@
+"""ctypes binding of libzarya.so: argument marshalling only.
+
+Every step of the slot-scoring path runs in the HIP kernels behind the C ABI
+declared in include/zarya.h; this module only checks tensor metadata, passes
+device pointers and torch's current HIP stream, and turns status codes into
+exceptions.  There is no fallback: if the library is missing, loading fails.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libzarya.so")
+
+OK = 0
+ERR_INVALID_ARGUMENT = 1
+ERR_UNSUPPORTED = 2
+ERR_WORKSPACE_TOO_SMALL = 3
+ERR_HIP = 4
+
+DTYPE_F32 = 0
+DTYPE_BF16 = 1
+PASS_DIFFUSION = 0
+PASS_AR_INFILL = 1
+CROSS_SLOT_NONE = 0
+CROSS_SLOT_CAUSAL = 1
+SLOT_CONF_FIRST_TOKEN = 0
+SLOT_CONF_MEAN = 1
+SELECT_THRESHOLD = 0
+SELECT_TOP_K = 1
+
+# every symbol include/zarya.h declares
+EXPORTS = (
+    "zarya_slot_attn_workspace_size",
+    "zarya_slot_attn",
+    "zarya_slot_confidence_workspace_size",
+    "zarya_slot_confidence",
+    "zarya_select_slots",
+    "zarya_status_string",
+    "zarya_last_error",
+    "zarya_version",
+)
+
+
+class SlotAttnDesc(ctypes.Structure):
+    _fields_ = [
+        ("batch", ctypes.c_int32),
+        ("n_q_heads", ctypes.c_int32),
+        ("n_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("prefix_len", ctypes.c_int32),
+        ("kv_capacity", ctypes.c_int32),
+        ("n_slots", ctypes.c_int32),
+        ("slot_len", ctypes.c_int32),
+        ("softmax_scale", ctypes.c_float),
+        ("pass_", ctypes.c_int32),
+        ("cross_slot", ctypes.c_int32),
+        ("dtype", ctypes.c_int32),
+        ("prefix_splits", ctypes.c_int32),
+    ]
+
+
+class ConfDesc(ctypes.Structure):
+    _fields_ = [
+        ("n_rows", ctypes.c_int32),
+        ("hidden", ctypes.c_int32),
+        ("vocab", ctypes.c_int32),
+        ("dtype", ctypes.c_int32),
+    ]
+
+
+class ZaryaError(RuntimeError):
+    def __init__(self, status, message):
+        super().__init__(f"{status_name(status)}: {message}")
+        self.status = status
+
+
+_lib = None
+
+
+def lib():
+    """Load libzarya.so once; raise if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(
+                f"{LIB_PATH} is missing: build it with `python -m paper_2609_19868_amd.build` "
+                "(the HIP library is the only implementation)"
+            )
+        L = ctypes.CDLL(LIB_PATH)
+        vp, sz, i32, f32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32, ctypes.c_float
+        L.zarya_slot_attn_workspace_size.argtypes = [ctypes.POINTER(SlotAttnDesc), ctypes.POINTER(sz)]
+        L.zarya_slot_attn_workspace_size.restype = ctypes.c_int
+        L.zarya_slot_attn.argtypes = [ctypes.POINTER(SlotAttnDesc), vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.zarya_slot_attn.restype = ctypes.c_int
+        L.zarya_slot_confidence_workspace_size.argtypes = [ctypes.POINTER(ConfDesc), ctypes.POINTER(sz)]
+        L.zarya_slot_confidence_workspace_size.restype = ctypes.c_int
+        L.zarya_slot_confidence.argtypes = [ctypes.POINTER(ConfDesc), vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.zarya_slot_confidence.restype = ctypes.c_int
+        L.zarya_select_slots.argtypes = [i32, i32, i32, vp, vp, i32, i32, f32, i32, vp, vp, vp, vp]
+        L.zarya_select_slots.restype = ctypes.c_int
+        L.zarya_status_string.argtypes = [ctypes.c_int]
+        L.zarya_status_string.restype = ctypes.c_char_p
+        L.zarya_last_error.argtypes = []
+        L.zarya_last_error.restype = ctypes.c_char_p
+        L.zarya_version.argtypes = []
+        L.zarya_version.restype = i32
+        _lib = L
+    return _lib
+
+
+def status_name(status):
+    return lib().zarya_status_string(status).decode()
+
+
+def check(status):
+    if status != OK:
+        raise ZaryaError(status, lib().zarya_last_error().decode())
+
+
+def slot_attn_workspace_size(desc: SlotAttnDesc) -> int:
+    n = ctypes.c_size_t(0)
+    check(lib().zarya_slot_attn_workspace_size(ctypes.byref(desc), ctypes.byref(n)))
+    return n.value
+
+
+def slot_confidence_workspace_size(desc: ConfDesc) -> int:
+    n = ctypes.c_size_t(0)
+    check(lib().zarya_slot_confidence_workspace_size(ctypes.byref(desc), ctypes.byref(n)))
+    return n.value

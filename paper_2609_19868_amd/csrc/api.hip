@@ -1,0 +1,346 @@
+// Host side of the libzarya C ABI: argument validation, workspace sizing,
+// work decomposition and kernel launches.  Nothing is launched unless every
+// argument passes validation.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <string>
+
+#include "kernels.hpp"
+#include "zarya.h"
+
+using namespace zarya;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+zarya_status fail(zarya_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+zarya_status hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return ZARYA_OK;
+  return fail(ZARYA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+constexpr int64_t kI32Max = 2147483647;
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// ------------------------------------------------------------- attention plan
+
+struct AttnPlan {
+  int T, G, R;
+  int n_split, tiles_per_split, n_prefix_tiles, n_rb;
+  int64_t rows_total;
+  size_t ws_bytes;
+};
+
+zarya_status check_attn_desc(const zarya_slot_attn_desc* d) {
+  if (!d) return fail(ZARYA_ERR_INVALID_ARGUMENT, "desc is NULL");
+  if (d->batch < 1 || d->n_q_heads < 1 || d->n_kv_heads < 1)
+    return fail(ZARYA_ERR_INVALID_ARGUMENT, "batch, n_q_heads and n_kv_heads must be >= 1");
+  if (d->n_q_heads % d->n_kv_heads != 0)
+    return fail(ZARYA_ERR_INVALID_ARGUMENT, "n_q_heads (%d) is not a multiple of n_kv_heads (%d)", d->n_q_heads,
+                d->n_kv_heads);
+  if (d->prefix_len < 0) return fail(ZARYA_ERR_INVALID_ARGUMENT, "prefix_len must be >= 0");
+  if (d->kv_capacity < d->prefix_len)
+    return fail(ZARYA_ERR_INVALID_ARGUMENT, "kv_capacity (%d) < prefix_len (%d)", d->kv_capacity, d->prefix_len);
+  if (d->n_slots < 1 || d->slot_len < 1) return fail(ZARYA_ERR_INVALID_ARGUMENT, "n_slots and slot_len must be >= 1");
+  if (!(isfinite(d->softmax_scale) && d->softmax_scale > 0.f))
+    return fail(ZARYA_ERR_INVALID_ARGUMENT, "softmax_scale must be finite and > 0");
+  if (d->pass != ZARYA_PASS_DIFFUSION && d->pass != ZARYA_PASS_AR_INFILL)
+    return fail(ZARYA_ERR_INVALID_ARGUMENT, "unknown pass %d", d->pass);
+  if (d->cross_slot != ZARYA_CROSS_SLOT_NONE && d->cross_slot != ZARYA_CROSS_SLOT_CAUSAL)
+    return fail(ZARYA_ERR_INVALID_ARGUMENT, "unknown cross_slot %d", d->cross_slot);
+  if (d->dtype != ZARYA_DTYPE_F32 && d->dtype != ZARYA_DTYPE_BF16)
+    return fail(ZARYA_ERR_INVALID_ARGUMENT, "unknown dtype %d", d->dtype);
+  if (d->prefix_splits < 0 || d->prefix_splits > 64)
+    return fail(ZARYA_ERR_INVALID_ARGUMENT, "prefix_splits must be in [0, 64]");
+  if (d->head_dim != 64 && d->head_dim != 128)
+    return fail(ZARYA_ERR_UNSUPPORTED, "head_dim %d is not supported (64 or 128)", d->head_dim);
+  const int64_t T = (int64_t)d->n_slots * d->slot_len;
+  const int64_t rows = (int64_t)d->batch * d->n_q_heads * T;
+  const int64_t cache_rows = (int64_t)d->batch * d->n_kv_heads * d->kv_capacity;
+  if (T > kI32Max || rows > kI32Max || cache_rows > kI32Max)
+    return fail(ZARYA_ERR_UNSUPPORTED, "problem too large: batch*heads*tokens must stay below 2^31");
+  return ZARYA_OK;
+}
+
+AttnPlan plan_attn(const zarya_slot_attn_desc* d) {
+  AttnPlan pl{};
+  pl.T = d->n_slots * d->slot_len;
+  pl.G = d->n_q_heads / d->n_kv_heads;
+  pl.R = pl.G * pl.T;
+  pl.rows_total = (int64_t)d->batch * d->n_q_heads * pl.T;
+  pl.n_rb = (pl.R + kAttnRowsPerBlock - 1) / kAttnRowsPerBlock;
+  pl.n_prefix_tiles = (d->prefix_len + kAttnKeysPerTile - 1) / kAttnKeysPerTile;
+  int ns = 1;
+  if (d->dtype == ZARYA_DTYPE_BF16 && pl.n_prefix_tiles > 0) {
+    if (d->prefix_splits > 0) {
+      ns = d->prefix_splits;
+    } else {
+      // aim for about two workgroups per compute unit, with at least two key
+      // tiles per split so the partial traffic stays small
+      const int64_t base = (int64_t)d->batch * d->n_kv_heads * pl.n_rb;
+      const int64_t want = (512 + base - 1) / base;
+      ns = (int)std::min<int64_t>(16, std::max<int64_t>(1, want));
+      ns = std::max(1, std::min(ns, pl.n_prefix_tiles / 2));
+    }
+    ns = std::min(ns, pl.n_prefix_tiles);
+    pl.tiles_per_split = (pl.n_prefix_tiles + ns - 1) / ns;
+    ns = (pl.n_prefix_tiles + pl.tiles_per_split - 1) / pl.tiles_per_split;
+  } else {
+    pl.tiles_per_split = pl.n_prefix_tiles;
+  }
+  pl.n_split = ns;
+  pl.ws_bytes = 0;
+  if (ns > 1) {
+    pl.ws_bytes = align256((size_t)ns * pl.rows_total * d->head_dim * 4) + align256((size_t)ns * pl.rows_total * 4);
+  }
+  return pl;
+}
+
+// ------------------------------------------------------------ confidence plan
+
+struct ConfPlan {
+  int n_vg, n_rt;
+  size_t ws_bytes;
+};
+
+zarya_status check_conf_desc(const zarya_conf_desc* d) {
+  if (!d) return fail(ZARYA_ERR_INVALID_ARGUMENT, "desc is NULL");
+  if (d->n_rows < 1 || d->hidden < 1 || d->vocab < 1)
+    return fail(ZARYA_ERR_INVALID_ARGUMENT, "n_rows, hidden and vocab must be >= 1");
+  if (d->dtype != ZARYA_DTYPE_F32 && d->dtype != ZARYA_DTYPE_BF16)
+    return fail(ZARYA_ERR_INVALID_ARGUMENT, "unknown dtype %d", d->dtype);
+  if (d->dtype == ZARYA_DTYPE_BF16 && d->hidden % 8 != 0)
+    return fail(ZARYA_ERR_UNSUPPORTED, "bf16 hidden size %d is not a multiple of 8", d->hidden);
+  if (d->dtype == ZARYA_DTYPE_F32 && d->hidden > 8192)
+    return fail(ZARYA_ERR_UNSUPPORTED, "f32 hidden size %d exceeds 8192", d->hidden);
+  if (d->dtype == ZARYA_DTYPE_F32 && d->n_rows > 65535)
+    return fail(ZARYA_ERR_UNSUPPORTED, "f32 path supports at most 65535 rows");
+  return ZARYA_OK;
+}
+
+ConfPlan plan_conf(const zarya_conf_desc* d) {
+  ConfPlan pl{};
+  if (d->dtype == ZARYA_DTYPE_BF16) {
+    pl.n_rt = (d->n_rows + kConfTileRows - 1) / kConfTileRows;
+    const int nblk = (d->vocab + 31) / 32;
+    // one workgroup per compute unit: split the vocabulary so that
+    // row tiles x vocabulary groups is about 256
+    pl.n_vg = std::max(1, std::min(nblk, 256 / pl.n_rt));
+  } else {
+    pl.n_rt = 1;
+    pl.n_vg = std::max(1, std::min(64, d->vocab / 2048));
+  }
+  pl.ws_bytes = 3 * align256((size_t)pl.n_vg * d->n_rows * 4);
+  return pl;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* zarya_status_string(zarya_status s) {
+  switch (s) {
+    case ZARYA_OK: return "ZARYA_OK";
+    case ZARYA_ERR_INVALID_ARGUMENT: return "ZARYA_ERR_INVALID_ARGUMENT";
+    case ZARYA_ERR_UNSUPPORTED: return "ZARYA_ERR_UNSUPPORTED";
+    case ZARYA_ERR_WORKSPACE_TOO_SMALL: return "ZARYA_ERR_WORKSPACE_TOO_SMALL";
+    case ZARYA_ERR_HIP: return "ZARYA_ERR_HIP";
+  }
+  return "ZARYA_STATUS_UNKNOWN";
+}
+
+const char* zarya_last_error(void) { return g_last_error.c_str(); }
+
+int32_t zarya_version(void) { return ZARYA_VERSION_MAJOR * 1000 + ZARYA_VERSION_MINOR; }
+
+zarya_status zarya_slot_attn_workspace_size(const zarya_slot_attn_desc* desc, size_t* bytes) {
+  if (!bytes) return fail(ZARYA_ERR_INVALID_ARGUMENT, "bytes is NULL");
+  zarya_status st = check_attn_desc(desc);
+  if (st != ZARYA_OK) return st;
+  *bytes = plan_attn(desc).ws_bytes;
+  return ZARYA_OK;
+}
+
+zarya_status zarya_slot_attn(const zarya_slot_attn_desc* d, const void* q, const void* k_cache, const void* v_cache,
+                             const void* k_slot, const void* v_slot, const uint8_t* slot_pass, void* out, float* lse,
+                             void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  zarya_status st = check_attn_desc(d);
+  if (st != ZARYA_OK) return st;
+  if (!q || !k_slot || !v_slot || !out) return fail(ZARYA_ERR_INVALID_ARGUMENT, "q, k_slot, v_slot and out are required");
+  if (d->prefix_len > 0 && (!k_cache || !v_cache))
+    return fail(ZARYA_ERR_INVALID_ARGUMENT, "k_cache and v_cache are required when prefix_len > 0");
+  const AttnPlan pl = plan_attn(d);
+  if (workspace_bytes < pl.ws_bytes)
+    return fail(ZARYA_ERR_WORKSPACE_TOO_SMALL, "workspace of %zu bytes is below the %zu required", workspace_bytes,
+                pl.ws_bytes);
+  if (pl.ws_bytes > 0 && !workspace) return fail(ZARYA_ERR_INVALID_ARGUMENT, "workspace is NULL");
+  (void)hipGetLastError();  // drop a stale error so the status below is ours
+
+  if (d->dtype == ZARYA_DTYPE_F32) {
+    AttnParams32 p{};
+    p.q = static_cast<const float*>(q);
+    p.k_cache = static_cast<const float*>(k_cache);
+    p.v_cache = static_cast<const float*>(v_cache);
+    p.k_slot = static_cast<const float*>(k_slot);
+    p.v_slot = static_cast<const float*>(v_slot);
+    p.slot_pass = slot_pass;
+    p.out = static_cast<float*>(out);
+    p.lse = lse;
+    p.B = d->batch;
+    p.Hq = d->n_q_heads;
+    p.Hkv = d->n_kv_heads;
+    p.P = d->prefix_len;
+    p.C = d->kv_capacity;
+    p.S = d->n_slots;
+    p.L = d->slot_len;
+    p.T = pl.T;
+    p.G = pl.G;
+    p.pass = d->pass;
+    p.cross = d->cross_slot;
+    p.scale = d->softmax_scale;
+    p.rows_total = (int)pl.rows_total;
+    return hip_status(launch_slot_attn_f32(p, d->head_dim, stream), "slot_attn f32 launch");
+  }
+
+  AttnParams p{};
+  p.q = static_cast<const uint16_t*>(q);
+  p.k_cache = static_cast<const uint16_t*>(k_cache);
+  p.v_cache = static_cast<const uint16_t*>(v_cache);
+  p.k_slot = static_cast<const uint16_t*>(k_slot);
+  p.v_slot = static_cast<const uint16_t*>(v_slot);
+  p.slot_pass = slot_pass;
+  p.out = static_cast<uint16_t*>(out);
+  p.lse = lse;
+  if (pl.n_split > 1) {
+    p.part_o = static_cast<float*>(workspace);
+    p.part_lse = reinterpret_cast<float*>(static_cast<char*>(workspace) +
+                                          align256((size_t)pl.n_split * pl.rows_total * d->head_dim * 4));
+  }
+  p.B = d->batch;
+  p.Hq = d->n_q_heads;
+  p.Hkv = d->n_kv_heads;
+  p.P = d->prefix_len;
+  p.C = d->kv_capacity;
+  p.S = d->n_slots;
+  p.L = d->slot_len;
+  p.T = pl.T;
+  p.G = pl.G;
+  p.R = pl.R;
+  p.pass = d->pass;
+  p.cross = d->cross_slot;
+  p.scale_log2 = d->softmax_scale * 1.4426950408889634f;
+  p.n_split = pl.n_split;
+  p.n_rb = pl.n_rb;
+  p.tiles_per_split = pl.tiles_per_split;
+  p.n_prefix_tiles = pl.n_prefix_tiles;
+  const int64_t items = (int64_t)d->batch * d->n_kv_heads * pl.n_split * pl.n_rb;
+  if (items > kI32Max / 2) return fail(ZARYA_ERR_UNSUPPORTED, "too many workgroups");
+  p.n_items = (int)items;
+  p.per_xcd = (p.n_items + 7) / 8;
+  p.rows_total = (int)pl.rows_total;
+  return hip_status(launch_slot_attn_bf16(p, d->head_dim, stream), "slot_attn bf16 launch");
+}
+
+zarya_status zarya_slot_confidence_workspace_size(const zarya_conf_desc* desc, size_t* bytes) {
+  if (!bytes) return fail(ZARYA_ERR_INVALID_ARGUMENT, "bytes is NULL");
+  zarya_status st = check_conf_desc(desc);
+  if (st != ZARYA_OK) return st;
+  *bytes = plan_conf(desc).ws_bytes;
+  return ZARYA_OK;
+}
+
+zarya_status zarya_slot_confidence(const zarya_conf_desc* d, const void* hidden, const void* w_vocab,
+                                   const int32_t* target_ids, float* max_prob, int32_t* argmax_id, float* lse,
+                                   float* target_prob, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  zarya_status st = check_conf_desc(d);
+  if (st != ZARYA_OK) return st;
+  if (!hidden || !w_vocab || !max_prob || !argmax_id)
+    return fail(ZARYA_ERR_INVALID_ARGUMENT, "hidden, w_vocab, max_prob and argmax_id are required");
+  const ConfPlan pl = plan_conf(d);
+  if (workspace_bytes < pl.ws_bytes)
+    return fail(ZARYA_ERR_WORKSPACE_TOO_SMALL, "workspace of %zu bytes is below the %zu required", workspace_bytes,
+                pl.ws_bytes);
+  if (!workspace) return fail(ZARYA_ERR_INVALID_ARGUMENT, "workspace is NULL");
+  (void)hipGetLastError();
+
+  const size_t part = align256((size_t)pl.n_vg * d->n_rows * 4);
+  ConfParams p{};
+  p.hidden = hidden;
+  p.w_vocab = w_vocab;
+  p.M = d->n_rows;
+  p.H = d->hidden;
+  p.V = d->vocab;
+  p.n_vg = pl.n_vg;
+  p.n_rt = pl.n_rt;
+  p.n_items = pl.n_vg * pl.n_rt;
+  p.per_xcd = (p.n_items + 7) / 8;
+  p.part_m = static_cast<float*>(workspace);
+  p.part_s = reinterpret_cast<float*>(static_cast<char*>(workspace) + part);
+  p.part_idx = reinterpret_cast<int*>(static_cast<char*>(workspace) + 2 * part);
+  hipError_t e = d->dtype == ZARYA_DTYPE_BF16 ? launch_slot_conf_bf16(p, stream) : launch_slot_conf_f32(p, stream);
+  if (e != hipSuccess) return hip_status(e, "slot_confidence launch");
+
+  ConfMergeParams mp{};
+  mp.part_m = p.part_m;
+  mp.part_s = p.part_s;
+  mp.part_idx = p.part_idx;
+  mp.n_vg = pl.n_vg;
+  mp.M = d->n_rows;
+  mp.H = d->hidden;
+  mp.V = d->vocab;
+  mp.bf16 = d->dtype == ZARYA_DTYPE_BF16;
+  mp.hidden = hidden;
+  mp.w_vocab = w_vocab;
+  mp.target_ids = target_ids;
+  mp.max_prob = max_prob;
+  mp.argmax_id = argmax_id;
+  mp.lse = lse;
+  mp.target_prob = target_prob;
+  return hip_status(launch_slot_conf_merge(mp, stream), "slot_confidence merge launch");
+}
+
+zarya_status zarya_select_slots(int32_t batch, int32_t n_slots, int32_t slot_len, const float* token_conf,
+                                const uint8_t* slot_open, int32_t conf_rule, int32_t rule, float threshold, int32_t k,
+                                float* slot_conf, int32_t* selected, int32_t* n_selected, hipStream_t stream) {
+  if (batch < 1 || batch > 65535) return fail(ZARYA_ERR_INVALID_ARGUMENT, "batch must be in [1, 65535]");
+  if (n_slots < 1) return fail(ZARYA_ERR_INVALID_ARGUMENT, "n_slots must be >= 1");
+  if (n_slots > 1024) return fail(ZARYA_ERR_UNSUPPORTED, "n_slots %d exceeds 1024", n_slots);
+  if (slot_len < 1) return fail(ZARYA_ERR_INVALID_ARGUMENT, "slot_len must be >= 1");
+  if (conf_rule != ZARYA_SLOT_CONF_FIRST_TOKEN && conf_rule != ZARYA_SLOT_CONF_MEAN)
+    return fail(ZARYA_ERR_INVALID_ARGUMENT, "unknown conf_rule %d", conf_rule);
+  if (rule != ZARYA_SELECT_THRESHOLD && rule != ZARYA_SELECT_TOP_K)
+    return fail(ZARYA_ERR_INVALID_ARGUMENT, "unknown rule %d", rule);
+  if (rule == ZARYA_SELECT_TOP_K && k < 0) return fail(ZARYA_ERR_INVALID_ARGUMENT, "k must be >= 0");
+  if (!token_conf || !slot_conf || !selected || !n_selected)
+    return fail(ZARYA_ERR_INVALID_ARGUMENT, "token_conf, slot_conf, selected and n_selected are required");
+  (void)hipGetLastError();
+  SelectParams p{};
+  p.B = batch;
+  p.S = n_slots;
+  p.L = slot_len;
+  p.token_conf = token_conf;
+  p.slot_open = slot_open;
+  p.conf_rule = conf_rule;
+  p.rule = rule;
+  p.threshold = threshold;
+  p.k = k;
+  p.slot_conf = slot_conf;
+  p.selected = selected;
+  p.n_selected = n_selected;
+  return hip_status(launch_select_slots(p, stream), "select_slots launch");
+}
+
+}  // extern "C"

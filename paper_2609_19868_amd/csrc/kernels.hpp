@@ -1,0 +1,98 @@
+// Kernel parameter blocks and launchers of libzarya (host <-> device contract).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace zarya {
+
+// bf16 slot attention.  Rows of a GQA group (G heads x T tokens) are
+// contiguous in q and out, so a group is addressed as one [R = G*T, D] block.
+struct AttnParams {
+  const uint16_t* q;        // [B, Hq, T, D]
+  const uint16_t* k_cache;  // [B, Hkv, C, D]
+  const uint16_t* v_cache;
+  const uint16_t* k_slot;  // [B, Hkv, T, D]
+  const uint16_t* v_slot;
+  const uint8_t* slot_pass;  // [B, S] or null
+  uint16_t* out;             // [B, Hq, T, D]
+  float* lse;                // [B, Hq, T] or null (natural log)
+  float* part_o;             // [n_split, rows_total, D]  (n_split > 1)
+  float* part_lse;           // [n_split, rows_total]     (n_split > 1, log2 units)
+  int B, Hq, Hkv, P, C, S, L, T, G, R;
+  int pass, cross;
+  float scale_log2;  // softmax scale * log2(e)
+  int n_split, n_rb, tiles_per_split, n_prefix_tiles;
+  int per_xcd, n_items;
+  int rows_total;  // B * Hq * T
+};
+
+struct AttnParams32 {
+  const float* q;
+  const float* k_cache;
+  const float* v_cache;
+  const float* k_slot;
+  const float* v_slot;
+  const uint8_t* slot_pass;
+  float* out;
+  float* lse;
+  int B, Hq, Hkv, P, C, S, L, T, G;
+  int pass, cross;
+  float scale;
+  int rows_total;
+};
+
+// LM-head confidence.  Partials are per (vocab group, row), in log2 units:
+// m = max of logit*log2(e), s = sum of 2^(x - m), idx = lowest id at the max.
+struct ConfParams {
+  const void* hidden;   // [M, H]
+  const void* w_vocab;  // [V, H]
+  int M, H, V;
+  int n_vg;        // vocabulary groups (partials per row)
+  int n_rt;        // row tiles (bf16 path)
+  int per_xcd, n_items;
+  float* part_m;   // [n_vg, M]
+  float* part_s;   // [n_vg, M]
+  int* part_idx;   // [n_vg, M]
+};
+
+struct ConfMergeParams {
+  const float* part_m;
+  const float* part_s;
+  const int* part_idx;
+  int n_vg, M, H, V;
+  int bf16;
+  const void* hidden;
+  const void* w_vocab;
+  const int32_t* target_ids;
+  float* max_prob;
+  int32_t* argmax_id;
+  float* lse;
+  float* target_prob;
+};
+
+struct SelectParams {
+  int B, S, L;
+  const float* token_conf;
+  const uint8_t* slot_open;
+  int conf_rule, rule;
+  float threshold;
+  int k;
+  float* slot_conf;
+  int32_t* selected;
+  int32_t* n_selected;
+};
+
+constexpr int kAttnKeysPerTile = 64;
+constexpr int kAttnRowsPerBlock = 128;
+constexpr int kConfTileV = 256;
+constexpr int kConfTileRows = 256;
+
+hipError_t launch_slot_attn_bf16(const AttnParams& p, int head_dim, hipStream_t stream);
+hipError_t launch_slot_attn_f32(const AttnParams32& p, int head_dim, hipStream_t stream);
+hipError_t launch_slot_conf_bf16(const ConfParams& p, hipStream_t stream);
+hipError_t launch_slot_conf_f32(const ConfParams& p, hipStream_t stream);
+hipError_t launch_slot_conf_merge(const ConfMergeParams& p, hipStream_t stream);
+hipError_t launch_select_slots(const SelectParams& p, hipStream_t stream);
+
+}  // namespace zarya

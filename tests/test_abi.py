@@ -1,0 +1,155 @@
+"""The C-ABI library: it loads, exports every declared symbol, and validates
+arguments on the host before any launch (CPU only: no call here reaches HIP)."""
+
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2609_19868_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "zarya.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(zarya_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_header_declares_the_binding_exports():
+    assert declared_functions() == sorted(_lib.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    L = _lib.lib()
+    out = subprocess.run(["nm", "-D", "--defined-only", _lib.LIB_PATH], capture_output=True, text=True, check=True).stdout
+    dyn = set(re.findall(r"\sT\s(\S+)", out))
+    for name in declared_functions():
+        assert name in dyn, f"{name} is not exported"
+        assert hasattr(L, name)
+
+
+def test_version_and_status_strings():
+    L = _lib.lib()
+    assert L.zarya_version() == 1
+    for code, name in [(0, "ZARYA_OK"), (1, "ZARYA_ERR_INVALID_ARGUMENT"), (2, "ZARYA_ERR_UNSUPPORTED"),
+                       (3, "ZARYA_ERR_WORKSPACE_TOO_SMALL"), (4, "ZARYA_ERR_HIP")]:
+        assert L.zarya_status_string(code).decode() == name
+
+
+def _desc(**kw):
+    base = dict(batch=2, n_q_heads=4, n_kv_heads=2, head_dim=128, prefix_len=100, kv_capacity=128, n_slots=4,
+                slot_len=8, softmax_scale=0.088, pass_=0, cross_slot=0, dtype=1, prefix_splits=0)
+    base.update(kw)
+    return _lib.SlotAttnDesc(**base)
+
+
+def _attn_status(desc, ptr=1, ws=None, ws_bytes=0):
+    p = ctypes.c_void_p(ptr) if ptr else None
+    return _lib.lib().zarya_slot_attn(ctypes.byref(desc), p, p, p, p, p, None, p, None, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("bad,code", [
+    (dict(batch=0), _lib.ERR_INVALID_ARGUMENT),
+    (dict(n_q_heads=3), _lib.ERR_INVALID_ARGUMENT),
+    (dict(n_kv_heads=0), _lib.ERR_INVALID_ARGUMENT),
+    (dict(prefix_len=-1), _lib.ERR_INVALID_ARGUMENT),
+    (dict(kv_capacity=50), _lib.ERR_INVALID_ARGUMENT),
+    (dict(n_slots=0), _lib.ERR_INVALID_ARGUMENT),
+    (dict(slot_len=0), _lib.ERR_INVALID_ARGUMENT),
+    (dict(softmax_scale=0.0), _lib.ERR_INVALID_ARGUMENT),
+    (dict(softmax_scale=float("nan")), _lib.ERR_INVALID_ARGUMENT),
+    (dict(pass_=2), _lib.ERR_INVALID_ARGUMENT),
+    (dict(cross_slot=5), _lib.ERR_INVALID_ARGUMENT),
+    (dict(dtype=7), _lib.ERR_INVALID_ARGUMENT),
+    (dict(prefix_splits=65), _lib.ERR_INVALID_ARGUMENT),
+    (dict(head_dim=96), _lib.ERR_UNSUPPORTED),
+    (dict(batch=1 << 20, n_q_heads=64, n_kv_heads=64), _lib.ERR_UNSUPPORTED),
+])
+def test_slot_attn_rejects_bad_descriptors(bad, code):
+    d = _desc(**bad)
+    assert _attn_status(d) == code
+    assert len(_lib.lib().zarya_last_error()) > 0
+    n = ctypes.c_size_t(0)
+    assert _lib.lib().zarya_slot_attn_workspace_size(ctypes.byref(d), ctypes.byref(n)) == code
+
+
+def test_slot_attn_rejects_null_pointers_and_small_workspace():
+    d = _desc()
+    assert _attn_status(d, ptr=0) == _lib.ERR_INVALID_ARGUMENT
+    need = _lib.slot_attn_workspace_size(d)
+    if need > 0:
+        assert _attn_status(d, ws=ctypes.c_void_p(1), ws_bytes=need - 1) == _lib.ERR_WORKSPACE_TOO_SMALL
+        assert _attn_status(d, ws=None, ws_bytes=need) == _lib.ERR_INVALID_ARGUMENT
+    # a prefix needs the cache pointers
+    p = ctypes.c_void_p(1)
+    assert _lib.lib().zarya_slot_attn(ctypes.byref(d), p, None, None, p, p, None, p, None, p, 1 << 40, None) == \
+        _lib.ERR_INVALID_ARGUMENT
+
+
+def test_slot_attn_workspace_sizes():
+    # one split needs no workspace; several splits need fp32 partials of O and LSE
+    d1 = _desc(prefix_splits=1)
+    assert _lib.slot_attn_workspace_size(d1) == 0
+    d4 = _desc(prefix_len=1024, kv_capacity=1024, prefix_splits=4)
+    rows = 2 * 4 * 32
+    assert _lib.slot_attn_workspace_size(d4) >= 4 * rows * (128 + 1) * 4
+    assert _lib.slot_attn_workspace_size(_desc(dtype=0)) == 0  # float32 path has no splits
+    assert _lib.slot_attn_workspace_size(_desc(prefix_len=0, kv_capacity=0)) == 0
+
+
+def _conf_status(desc, ptr=1, ws_bytes=1 << 40):
+    p = ctypes.c_void_p(ptr) if ptr else None
+    return _lib.lib().zarya_slot_confidence(ctypes.byref(desc), p, p, None, p, p, None, None, p, ws_bytes, None)
+
+
+@pytest.mark.parametrize("bad,code", [
+    (dict(n_rows=0), _lib.ERR_INVALID_ARGUMENT),
+    (dict(hidden=0), _lib.ERR_INVALID_ARGUMENT),
+    (dict(vocab=0), _lib.ERR_INVALID_ARGUMENT),
+    (dict(dtype=3), _lib.ERR_INVALID_ARGUMENT),
+    (dict(hidden=1001), _lib.ERR_UNSUPPORTED),
+    (dict(dtype=0, hidden=10000), _lib.ERR_UNSUPPORTED),
+])
+def test_slot_confidence_rejects_bad_descriptors(bad, code):
+    base = dict(n_rows=64, hidden=1024, vocab=151936, dtype=1)
+    base.update(bad)
+    assert _conf_status(_lib.ConfDesc(**base)) == code
+
+
+def test_slot_confidence_workspace_checks():
+    d = _lib.ConfDesc(n_rows=1024, hidden=1024, vocab=151936, dtype=1)
+    need = _lib.slot_confidence_workspace_size(d)
+    assert need >= 64 * 1024 * 12
+    assert _conf_status(d, ws_bytes=need - 1) == _lib.ERR_WORKSPACE_TOO_SMALL
+    assert _conf_status(d, ptr=0) == _lib.ERR_INVALID_ARGUMENT
+
+
+@pytest.mark.parametrize("args,code", [
+    (dict(batch=0), _lib.ERR_INVALID_ARGUMENT),
+    (dict(n_slots=0), _lib.ERR_INVALID_ARGUMENT),
+    (dict(n_slots=2048), _lib.ERR_UNSUPPORTED),
+    (dict(slot_len=0), _lib.ERR_INVALID_ARGUMENT),
+    (dict(conf_rule=2), _lib.ERR_INVALID_ARGUMENT),
+    (dict(rule=9), _lib.ERR_INVALID_ARGUMENT),
+    (dict(rule=1, k=-1), _lib.ERR_INVALID_ARGUMENT),
+    (dict(ptr=0), _lib.ERR_INVALID_ARGUMENT),
+])
+def test_select_slots_rejects_bad_arguments(args, code):
+    a = dict(batch=4, n_slots=8, slot_len=4, conf_rule=0, rule=0, threshold=0.9, k=1, ptr=1)
+    a.update(args)
+    p = ctypes.c_void_p(a["ptr"]) if a["ptr"] else None
+    st = _lib.lib().zarya_select_slots(a["batch"], a["n_slots"], a["slot_len"], p, None, a["conf_rule"], a["rule"],
+                                       a["threshold"], a["k"], p, p, p, None)
+    assert st == code
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(_lib, "_lib", None)
+    monkeypatch.setattr(_lib, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(ImportError):
+        _lib.lib()

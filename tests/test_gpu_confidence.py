@@ -1,0 +1,123 @@
+"""slot_confidence on the GPU (through the C ABI) against the float64 oracle.
+
+Tolerances: max_prob |diff| <= 1e-3 and <= 1e-3 * max_prob; lse |diff| <= 1e-3;
+target_prob relative 1e-3; argmax ids exact wherever the oracle's top-2 logit
+gap is >= 1e-3, elsewhere the GPU's id must be within 1e-3 of the maximal
+logit (float32 path: 1e-4 in place of 1e-3).  Planted rows give max_prob
+values across (1/V, 1) so the max_prob checks are not vacuous.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as W
+from gpu_helpers import check_conf, require_gpu, say, to_dev
+
+import paper_2609_19868_amd as Z
+
+pytestmark = pytest.mark.gpu
+
+
+def _planted(M, V, n, seed):
+    rng = np.random.default_rng(seed)
+    rows = rng.choice(M, size=min(n, M), replace=False)
+    vids = rng.integers(0, V, size=len(rows))
+    alphas = rng.uniform(0.0, 120.0, size=len(rows))
+    return rows, vids, alphas
+
+
+def _run_and_check(wl, dev, n_rows=None, plant=None, what="", sample=None):
+    c = W.confidence_inputs(wl, n_rows=n_rows, plant=plant)
+    hd = to_dev(c["hidden"], wl.dtype, dev)
+    wd = to_dev(c["w_vocab"], wl.dtype, dev)
+    td = torch.from_numpy(c["target_ids"]).to(dev)
+    say(f"slot_confidence {what}")
+    res = Z.slot_confidence(hd, wd, target_ids=td)
+    torch.cuda.synchronize()
+    rows = np.arange(hd.shape[0]) if sample is None else sample
+    hf = W.as_f64(c["hidden"][rows], wl.dtype)
+    wf = W.as_f64(c["w_vocab"], wl.dtype)
+    ref = oracle.slot_confidence(hf, wf, target_ids=c["target_ids"][rows])
+    n_near = check_conf(res, ref, rows=rows, what=what, f32=wl.dtype == "f32",
+                        logit_of=lambda i, v: float(hf[i] @ wf[v]))
+    return res, ref, n_near
+
+
+def test_tiny_fp32():
+    dev = require_gpu()
+    wl = W.WORKLOADS["tiny"]
+    _run_and_check(wl, dev, plant=_planted(wl.M, wl.vocab, 6, 1), what="tiny f32")
+
+
+SMALL = [
+    ("m300_v5000_h256", dict(batch=1, n_slots=60, slot_len=5, hidden=256, vocab=5000)),
+    ("m40_v2049_h136", dict(batch=1, n_slots=8, slot_len=5, hidden=136, vocab=2049)),
+    ("m1_v100_h64", dict(batch=1, n_slots=1, slot_len=1, hidden=64, vocab=100)),
+    ("m513_v33000_h1024", dict(batch=1, n_slots=27, slot_len=19, hidden=1024, vocab=33000)),
+]
+
+
+@pytest.mark.parametrize("name,over", SMALL, ids=[s[0] for s in SMALL])
+def test_bf16_small_shapes(name, over):
+    dev = require_gpu()
+    wl = W.WORKLOADS["qwen0.6b"].replace(**over, seed=91)
+    res, ref, _ = _run_and_check(wl, dev, plant=_planted(wl.M, wl.vocab, wl.M // 3 + 1, 2), what=name)
+    mp = res["max_prob"].cpu().numpy()
+    if wl.M >= 20:
+        assert mp.max() > 0.9 and mp.min() < 0.01, "planted rows should span the probability range"
+
+
+def test_bf16_zero_hidden_rows():
+    dev = require_gpu()
+    V, H = 3000, 128
+    w = to_dev(W.bf16_bits(np.random.default_rng(3).standard_normal((V, H)).astype(np.float32) * 0.02), "bf16", dev)
+    h = torch.zeros((5, H), dtype=torch.bfloat16, device=dev)
+    res = Z.slot_confidence(h, w)
+    torch.cuda.synchronize()
+    assert torch.all(res["argmax"] == 0)
+    np.testing.assert_allclose(res["lse"].cpu().numpy(), np.log(V), atol=1e-5)
+    np.testing.assert_allclose(res["max_prob"].cpu().numpy(), 1.0 / V, rtol=1e-5)
+
+
+def test_bf16_ties_take_the_lowest_id():
+    dev = require_gpu()
+    rng = np.random.default_rng(8)
+    V, H = 4000, 64
+    w = W.bf16_bits(rng.standard_normal((V, H)).astype(np.float32) * 0.02)
+    h = W.bf16_bits(rng.standard_normal((4, H)).astype(np.float32))
+    # duplicate a strongly aligned row at several ids: equal maxima
+    target = w[123].copy()
+    for v in (123, 124, 2000, 3999):
+        w[v] = target
+    h[:] = W.bf16_bits(W.bf16_to_f32(target) * 50.0)
+    res = Z.slot_confidence(to_dev(h, "bf16", dev), to_dev(w, "bf16", dev))
+    torch.cuda.synchronize()
+    assert torch.all(res["argmax"] == 123), res["argmax"]
+
+
+def test_bf16_bitwise_deterministic():
+    dev = require_gpu()
+    wl = W.WORKLOADS["qwen0.6b"].replace(batch=1, n_slots=64, slot_len=5, hidden=512, vocab=20000, seed=92)
+    c = W.confidence_inputs(wl)
+    hd, wd = to_dev(c["hidden"], "bf16", dev), to_dev(c["w_vocab"], "bf16", dev)
+    a = Z.slot_confidence(hd, wd)
+    b = Z.slot_confidence(hd, wd)
+    torch.cuda.synchronize()
+    for k in ("max_prob", "argmax", "lse"):
+        assert torch.equal(a[k], b[k]), k
+
+
+@pytest.mark.parametrize("name", ["qwen0.6b", "qwen1.7b", "qwen4b"])
+def test_full_size_sampled(name):
+    """Full vocabulary 151936 and full row count in the benchmark's launch
+    configuration; the oracle checks a sample of rows (all vocab entries each)."""
+    dev = require_gpu()
+    wl = W.WORKLOADS[name]
+    rng = np.random.default_rng(11)
+    sample = np.unique(np.concatenate([rng.choice(wl.M, 48, replace=False), [0, wl.M - 1]]))
+    plant = _planted(wl.M, wl.vocab, 16, 3)
+    sample = np.unique(np.concatenate([sample, plant[0]]))
+    say(f"slot_confidence full {name}: generating inputs")
+    _run_and_check(wl, dev, plant=plant, what=f"full {name}", sample=sample)

@@ -1,0 +1,169 @@
+"""slot_attn on the GPU (through the C ABI) against the float64 oracle.
+
+Tolerances: bf16 outputs |diff| <= 2e-2 + 1e-2*|ref| elementwise, relative L2
+per (batch, head) <= 1e-2 (the bf16 rounding of P and of O gives ~3e-3), LSE
+|diff| <= 1e-3; float32 path: 1e-4 + 1e-4*|ref| and LSE 1e-4.  Inputs are the
+seeded workloads (bf16 bits shared by both sides), also with queries scaled by
+4 ("peaked") so that the softmax is far from uniform.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as W
+from gpu_helpers import attn_inputs_dev, check_attn, require_gpu, say, to_dev, to_f64
+
+import paper_2609_19868_amd as Z
+
+pytestmark = pytest.mark.gpu
+
+PASSES = [(Z.PASS_DIFFUSION, "diffusion"), (Z.PASS_AR_INFILL, "ar_infill")]
+
+
+def _run(xd, wl, pass_, cross=Z.CROSS_SLOT_NONE, slot_pass=None, splits=0):
+    out, lse = Z.slot_attn(xd["q"], xd["k_cache"] if wl.capacity else None, xd["v_cache"] if wl.capacity else None,
+                           xd["k_slot"], xd["v_slot"], wl.n_slots, wl.slot_len, pass_=pass_, cross_slot=cross,
+                           slot_pass=slot_pass, prefix_len=wl.prefix_len, softmax_scale=wl.scale,
+                           prefix_splits=splits)
+    torch.cuda.synchronize()
+    return out, lse
+
+
+def _oracle(xf, wl, pass_, cross=oracle.CROSS_SLOT_NONE, slot_pass=None):
+    return oracle.slot_attention(xf["q"], xf["k_cache"], xf["v_cache"], xf["k_slot"], xf["v_slot"], wl.prefix_len,
+                                 wl.n_slots, wl.slot_len, wl.scale, pass_, cross_slot=cross, slot_pass=slot_pass)
+
+
+def test_tiny_fp32_both_passes():
+    dev = require_gpu()
+    wl = W.WORKLOADS["tiny"]
+    xd, xf = attn_inputs_dev(wl, dev)
+    for pass_, name in PASSES:
+        say(f"slot_attn tiny f32 {name}")
+        out, lse = _run(xd, wl, pass_)
+        O, L = _oracle(xf, wl, pass_)
+        check_attn(to_f64(out), to_f64(lse), O, L, "f32", f"tiny {name}")
+
+
+SMALL_BF16 = [
+    # name, workload overrides: several key tiles, ragged prefix and token counts
+    ("p300_s5l7", dict(batch=2, n_q_heads=4, n_kv_heads=2, prefix_len=300, kv_capacity=320, n_slots=5, slot_len=7)),
+    ("g4_two_row_blocks", dict(batch=1, n_q_heads=8, n_kv_heads=2, prefix_len=200, n_slots=6, slot_len=8)),
+    ("no_prefix", dict(batch=2, n_q_heads=2, n_kv_heads=1, prefix_len=0, n_slots=9, slot_len=5)),
+    ("l1_decode", dict(batch=2, n_q_heads=4, n_kv_heads=4, prefix_len=130, n_slots=16, slot_len=1)),
+    ("one_slot", dict(batch=1, n_q_heads=4, n_kv_heads=1, prefix_len=64, n_slots=1, slot_len=33)),
+    ("d64", dict(batch=2, n_q_heads=4, n_kv_heads=2, head_dim=64, prefix_len=257, n_slots=4, slot_len=6)),
+]
+
+
+@pytest.mark.parametrize("name,over", SMALL_BF16, ids=[c[0] for c in SMALL_BF16])
+@pytest.mark.parametrize("q_scale", [1.0, 4.0], ids=["normal", "peaked"])
+def test_bf16_small_shapes(name, over, q_scale):
+    dev = require_gpu()
+    wl = W.WORKLOADS["qwen0.6b"].replace(**over, hidden=0, vocab=0, seed=77)
+    xd, xf = attn_inputs_dev(wl, dev, q_scale=q_scale)
+    for pass_, pname in PASSES:
+        say(f"slot_attn bf16 {name} q_scale={q_scale} {pname}")
+        out, lse = _run(xd, wl, pass_)
+        O, L = _oracle(xf, wl, pass_)
+        check_attn(to_f64(out), to_f64(lse), O, L, "bf16", f"{name} {pname}")
+
+
+def test_bf16_per_slot_pass_and_cross_causal():
+    dev = require_gpu()
+    wl = W.WORKLOADS["qwen0.6b"].replace(batch=2, n_q_heads=4, n_kv_heads=2, prefix_len=150, n_slots=6, slot_len=8,
+                                         hidden=0, vocab=0, seed=78)
+    xd, xf = attn_inputs_dev(wl, dev)
+    sp = (np.random.default_rng(4).random((2, 6)) < 0.5).astype(np.uint8)
+    for cross in (Z.CROSS_SLOT_NONE, Z.CROSS_SLOT_CAUSAL):
+        say(f"slot_attn bf16 slot_pass cross={cross}")
+        out, lse = _run(xd, wl, Z.PASS_DIFFUSION, cross=cross, slot_pass=torch.from_numpy(sp).to(dev))
+        O, L = _oracle(xf, wl, oracle.PASS_DIFFUSION, cross=cross, slot_pass=sp)
+        check_attn(to_f64(out), to_f64(lse), O, L, "bf16", f"slot_pass cross={cross}")
+
+
+def test_bf16_split_counts_agree_and_runs_are_bitwise_identical():
+    dev = require_gpu()
+    wl = W.WORKLOADS["qwen0.6b"].replace(batch=2, prefix_len=1000, hidden=0, vocab=0, seed=79)
+    xd, xf = attn_inputs_dev(wl, dev)
+    O, L = _oracle(xf, wl, oracle.PASS_DIFFUSION)
+    outs = {}
+    for splits in (1, 2, 4, 8):
+        say(f"slot_attn bf16 splits={splits}")
+        out, lse = _run(xd, wl, Z.PASS_DIFFUSION, splits=splits)
+        check_attn(to_f64(out), to_f64(lse), O, L, "bf16", f"splits={splits}")
+        out2, lse2 = _run(xd, wl, Z.PASS_DIFFUSION, splits=splits)
+        assert torch.equal(out.view(torch.int16), out2.view(torch.int16)), "rerun differs"
+        assert torch.equal(lse, lse2), "rerun LSE differs"
+        outs[splits] = (to_f64(out), to_f64(lse))
+    for splits in (2, 4, 8):
+        # each split rounds its probabilities to bf16 against its own running
+        # maximum, so splits agree to that rounding (2^-9 relative per term of a
+        # convex combination of |v| <= ~5), not bit for bit; LSE is float32 only
+        d = np.abs(outs[splits][0] - outs[1][0])
+        assert d.max() <= 4e-3 and d.mean() <= 2e-4, f"split {splits} vs 1: max {d.max():.3e} mean {d.mean():.3e}"
+        assert np.abs(outs[splits][1] - outs[1][1]).max() < 1e-5
+
+
+def test_bf16_outputs_stay_inside_their_buffers():
+    dev = require_gpu()
+    wl = W.WORKLOADS["qwen0.6b"].replace(batch=1, n_q_heads=4, n_kv_heads=2, prefix_len=100, n_slots=3, slot_len=5,
+                                         hidden=0, vocab=0, seed=80)
+    xd, xf = attn_inputs_dev(wl, dev)
+    B, Hq, T, D = xd["q"].shape
+    n = B * Hq * T * D
+    guard = 4096
+    buf = torch.full((n + 2 * guard,), 7.0, dtype=torch.bfloat16, device=dev)
+    lbuf = torch.full((B * Hq * T + 2 * guard,), 7.0, dtype=torch.float32, device=dev)
+    out = buf[guard:guard + n].view(B, Hq, T, D)
+    lse = lbuf[guard:guard + B * Hq * T].view(B, Hq, T)
+    for splits in (1, 3):
+        say(f"slot_attn guard canaries splits={splits}")
+        Z.slot_attn(xd["q"], xd["k_cache"], xd["v_cache"], xd["k_slot"], xd["v_slot"], wl.n_slots, wl.slot_len,
+                    prefix_len=wl.prefix_len, out=out, lse=lse, prefix_splits=splits)
+        torch.cuda.synchronize()
+        assert torch.all(buf[:guard] == 7.0) and torch.all(buf[guard + n:] == 7.0)
+        assert torch.all(lbuf[:guard] == 7.0) and torch.all(lbuf[guard + B * Hq * T:] == 7.0)
+    O, L = _oracle(xf, wl, oracle.PASS_DIFFUSION)
+    check_attn(to_f64(out), to_f64(lse), O, L, "bf16", "guarded")
+
+
+@pytest.mark.parametrize("name", ["qwen0.6b", "qwen1.7b", "qwen4b"])
+def test_full_size_sampled(name):
+    """Full workload shapes in the launch configuration the benchmark times; the
+    oracle checks a sample of (batch, head) pairs, every token of each."""
+    dev = require_gpu()
+    wl = W.WORKLOADS[name].replace(hidden=0, vocab=0)
+    say(f"slot_attn full {name}: generating inputs")
+    x = W.attention_inputs(wl)
+    xd = {k: to_dev(v, wl.dtype, dev) for k, v in x.items()}
+    rng = np.random.default_rng(5)
+    picks = [(int(rng.integers(wl.batch)), int(rng.integers(wl.n_q_heads))) for _ in range(3)]
+    picks.append((wl.batch - 1, wl.n_q_heads - 1))
+    G = wl.n_q_heads // wl.n_kv_heads
+    for pass_, pname in PASSES:
+        say(f"slot_attn full {name} {pname}")
+        out, lse = _run(xd, wl, pass_)
+        Og, Lg = to_f64(out), to_f64(lse)
+        for b, h in picks:
+            g = h // G
+            sub = wl.replace(batch=1, n_q_heads=1, n_kv_heads=1)
+            xf = {
+                "q": W.as_f64(x["q"][b:b + 1, h:h + 1], "bf16"),
+                "k_cache": W.as_f64(x["k_cache"][b:b + 1, g:g + 1], "bf16"),
+                "v_cache": W.as_f64(x["v_cache"][b:b + 1, g:g + 1], "bf16"),
+                "k_slot": W.as_f64(x["k_slot"][b:b + 1, g:g + 1], "bf16"),
+                "v_slot": W.as_f64(x["v_slot"][b:b + 1, g:g + 1], "bf16"),
+            }
+            O, L = _oracle(xf, sub, pass_)
+            check_attn(Og[b:b + 1, h:h + 1], Lg[b:b + 1, h:h + 1], O, L, "bf16", f"{name} {pname} b={b} h={h}")
+        # properties that hold everywhere: finite, and the last token of a slot agrees across passes
+        assert np.isfinite(Og).all() and np.isfinite(Lg).all()
+        if pass_ == Z.PASS_DIFFUSION:
+            last_diff = (Og, Lg)
+        else:
+            last = np.arange(wl.n_slots) * wl.slot_len + wl.slot_len - 1
+            assert np.abs(Og[:, :, last] - last_diff[0][:, :, last]).max() <= 1e-2
+            assert np.abs(Lg[:, :, last] - last_diff[1][:, :, last]).max() <= 1e-4
