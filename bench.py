@@ -1,0 +1,302 @@
+#!/usr/bin/env python3
+"""Benchmark one slot-scoring step of Zarya's slotted speculative decoding on one MI355X.
+
+A step (Sec. 5.2 of the paper: draft phase, slot confidence, slot selection)
+is, on one batch of synthetic input already resident in HBM:
+
+  1. zarya_slot_attn        DIFFUSION pass (draft) over the prefix cache
+  2. zarya_slot_confidence  LM-head confidence of every draft token
+  3. zarya_select_slots     threshold 0.9 on the first-token confidence
+
+Workload (default): qwen0.6b -- B=16, Hq/Hkv=16/8, D=128, P=2048, S=8, L=8,
+H=1024, V=151936, bf16.  Three copies of the inputs are rotated so that
+neither the KV cache nor the LM head is served from the 256 MB Infinity Cache.
+
+Prints one JSON line: steps/s (value), draft tokens/s, per-call times from HIP
+events on the launch stream, the roofline of the dominant kernel
+(slot_confidence against the bf16 MFMA peak) and of slot_attn (against HBM),
+and the float64 CPU oracle timed on the host cores as a reference baseline.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBPS = 8000.0
+PEAK_BF16_TFLOPS = 2500.0
+METRIC = "slot-scoring steps/s, draft tokens/s; slot_attn HBM GB/s & conf MFMA % @1 MI355X"
+COUNTERS = os.path.join(ROOT, "profiles", "hbm_traffic_counters.md")
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def conf_source_hash():
+    """sha256 of the sources the confidence kernel is built from (ties the
+    committed counter readings to the kernel version they were taken on)."""
+    h = hashlib.sha256()
+    for f in ("slot_conf.hip", "common.hpp", "kernels.hpp"):
+        with open(os.path.join(ROOT, "paper_2609_19868_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload):
+    """HBM bytes per slot_confidence launch from the committed rocprofv3
+    counter summary, or None when absent or taken on other kernel sources."""
+    if not os.path.exists(COUNTERS):
+        return None
+    text = open(COUNTERS).read()
+    m = re.search(r"^source_sha256:\s*(\S+)", text, re.M)
+    t = re.search(rf"^traffic_bytes\[{re.escape(workload)}\]:\s*([0-9.eE+]+)", text, re.M)
+    if not m or not t or m.group(1) != conf_source_hash():
+        return None
+    return float(t.group(1))
+
+
+def cpu_baseline(wl, x, c):
+    """The float64 oracle as it stands, on this host's cores: the whole step."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    import oracle
+    import workloads as W
+
+    xf = {k: W.as_f64(v, wl.dtype) for k, v in x.items()}
+    hf = W.as_f64(c["hidden"], wl.dtype)
+    wf = W.as_f64(c["w_vocab"], wl.dtype)
+    times = []
+    for rep in range(3):
+        t0 = time.perf_counter()
+        oracle.slot_attention(xf["q"], xf["k_cache"], xf["v_cache"], xf["k_slot"], xf["v_slot"], wl.prefix_len,
+                              wl.n_slots, wl.slot_len, wl.scale, oracle.PASS_DIFFUSION)
+        r = oracle.slot_confidence(hf, wf)
+        oracle.select_slots(r["max_prob"].reshape(wl.batch, wl.n_slots, wl.slot_len).astype(np.float32), None,
+                            oracle.CONF_FIRST_TOKEN, oracle.SELECT_THRESHOLD, 0.9, 1)
+        times.append(time.perf_counter() - t0)
+        log(f"cpu oracle step {rep}: {times[-1]:.2f} s")
+    threads = max([d.get("num_threads", 1) for d in threadpool_info()] + [1])
+    t = statistics.median(times)
+    return {
+        "value": 1.0 / t,
+        "unit": "steps/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": "the whole step (attention of all 16x16 heads x 64 tokens, confidence of all 1024 rows over "
+                  "151936 ids, selection), float64 numpy, median of 3 runs; "
+                  f"host has {len(os.sched_getaffinity(0))} usable cores, BLAS threads {threads}",
+        "seconds_per_step": t,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="qwen0.6b", choices=["qwen0.6b", "qwen1.7b", "qwen4b"])
+    ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the CPU oracle leg")
+    ap.add_argument("--no-extras", action="store_true", help="skip the AR_INFILL and layout-attention timings")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures the slot-scoring step on one GPU only; the multi-GPU sharding is designed "
+              "but not built (run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import workloads as W
+    import paper_2609_19868_amd as Z
+
+    dev = torch.device("cuda:0")
+    wl = W.WORKLOADS[args.workload]
+    B, Hq, Hkv, D, P, S, L, H, V = (wl.batch, wl.n_q_heads, wl.n_kv_heads, wl.head_dim, wl.prefix_len, wl.n_slots,
+                                    wl.slot_len, wl.hidden, wl.vocab)
+    T, M = wl.T, wl.M
+
+    log(f"generating {wl.name} inputs")
+    x = W.attention_inputs(wl)
+    c = W.confidence_inputs(wl)
+
+    def dev_bf16(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    base = {k: dev_bf16(v) for k, v in x.items()}
+    base["hidden"] = dev_bf16(c["hidden"])
+    base["w_vocab"] = dev_bf16(c["w_vocab"])
+    n_sets = 3
+    sets = [base] + [{k: v.clone() for k, v in base.items()} for _ in range(n_sets - 1)]
+
+    out = torch.empty((B, Hq, T, D), dtype=torch.bfloat16, device=dev)
+    lse = torch.empty((B, Hq, T), dtype=torch.float32, device=dev)
+    desc = Z.slot_attn_desc(base["q"], base["k_cache"], base["k_slot"], S, L, Z.PASS_DIFFUSION)
+    from paper_2609_19868_amd import _lib
+
+    attn_ws = torch.empty(max(1, _lib.slot_attn_workspace_size(desc)), dtype=torch.uint8, device=dev)
+    conf_out = {
+        "max_prob": torch.empty(M, dtype=torch.float32, device=dev),
+        "argmax": torch.empty(M, dtype=torch.int32, device=dev),
+        "lse": torch.empty(M, dtype=torch.float32, device=dev),
+    }
+    conf_ws = torch.empty(_lib.slot_confidence_workspace_size(_lib.ConfDesc(n_rows=M, hidden=H, vocab=V, dtype=1)),
+                          dtype=torch.uint8, device=dev)
+    sel_out = (torch.empty((B, S), dtype=torch.float32, device=dev), torch.empty((B, S), dtype=torch.int32, device=dev),
+               torch.empty((B,), dtype=torch.int32, device=dev))
+
+    def step(s, pass_, evs=None):
+        if evs:
+            evs[0].record()
+        Z.slot_attn(s["q"], s["k_cache"], s["v_cache"], s["k_slot"], s["v_slot"], S, L, pass_=pass_, out=out, lse=lse,
+                    workspace=attn_ws)
+        if evs:
+            evs[1].record()
+        Z.slot_confidence(s["hidden"], s["w_vocab"], out=conf_out, workspace=conf_ws)
+        if evs:
+            evs[2].record()
+        Z.select_slots(conf_out["max_prob"].view(B, S, L), None, Z.SLOT_CONF_FIRST_TOKEN, Z.SELECT_THRESHOLD, 0.9, 1,
+                       out=sel_out)
+        if evs:
+            evs[3].record()
+
+    def timed(pass_, K, Wm):
+        for i in range(Wm):
+            step(sets[i % n_sets], pass_)
+        torch.cuda.synchronize()
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+        t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t_start.record()
+        for i in range(K):
+            step(sets[i % n_sets], pass_, evs[i])
+        t_end.record()
+        torch.cuda.synchronize()
+        total_ms = t_start.elapsed_time(t_end)
+        per = [[e[j].elapsed_time(e[j + 1]) for j in range(3)] for e in evs]
+        return total_ms / K, [statistics.mean(p[j] for p in per) for j in range(3)], \
+            [statistics.median(p[j] for p in per) for j in range(3)]
+
+    log(f"timing {args.steps} steps after {args.warmup} warm-up steps (DIFFUSION pass)")
+    ms_step, mean_ms, med_ms = timed(Z.PASS_DIFFUSION, args.steps, args.warmup)
+    attn_ms, conf_ms, sel_ms = mean_ms
+    log(f"step {ms_step * 1e3:.1f} us: slot_attn {attn_ms * 1e3:.1f} us, slot_confidence {conf_ms * 1e3:.1f} us, "
+        f"select_slots {sel_ms * 1e3:.1f} us")
+
+    # algorithmic work (what the method must move / compute once)
+    attn_bytes = (2 * B * Hkv * P * D * 2  # prefix K and V, once per GQA group
+                  + 2 * B * Hq * T * D * 2  # Q in, O out
+                  + 2 * B * Hkv * T * D * 2  # the draft tokens' own K and V
+                  + B * Hq * T * 4)  # LSE
+    conf_flops = 2.0 * M * V * H
+    conf_tflops = conf_flops / (conf_ms * 1e-3) / 1e12
+    attn_gbps = attn_bytes / (attn_ms * 1e-3) / 1e9
+    traffic = measured_traffic(wl.name)
+
+    result = {
+        "metric": METRIC,
+        "value": 1e3 / ms_step,
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) activations and KV cache, N(0,0.02^2) LM head, rounded to bf16)",
+        "config": {
+            "workload": f"{wl.name}: B={B} Hq/Hkv={Hq}/{Hkv} D={D} P={P} S={S} L={L} H={H} V={V}; "
+                        "step = slot_attn (DIFFUSION) + slot_confidence + select_slots (threshold 0.9)",
+            "batch": B, "prefix_len": P, "n_slots": S, "slot_len": L, "hidden": H, "vocab": V,
+            "parallelism": "single GPU",
+        },
+        "draft_tokens_per_s": B * S * L * 1e3 / ms_step,
+        "kernel_us": {"slot_attn": attn_ms * 1e3, "slot_confidence": conf_ms * 1e3, "select_slots": sel_ms * 1e3},
+        "kernel_us_median": {"slot_attn": med_ms[0] * 1e3, "slot_confidence": med_ms[1] * 1e3,
+                             "select_slots": med_ms[2] * 1e3},
+        "roofline": {
+            "bound": "mfma",
+            "kernel": "slot_confidence (GEMM + fused reduction, plus its partial-merge kernel)",
+            "achieved": conf_tflops,
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": conf_tflops / PEAK_BF16_TFLOPS,
+            "traffic": traffic,
+            "algorithmic_flops_per_launch": conf_flops,
+        },
+        "roofline_slot_attn": {
+            "bound": "hbm",
+            "achieved": attn_gbps,
+            "peak": PEAK_HBM_GBPS,
+            "unit": "GB/s",
+            "frac": attn_gbps / PEAK_HBM_GBPS,
+            "algorithmic_bytes_per_launch": attn_bytes,
+            "prefix_splits": max(1, round(_lib.slot_attn_workspace_size(desc) / (B * Hq * T * (D + 1) * 4))),
+        },
+    }
+
+    if not args.no_extras:
+        log("timing the AR_INFILL (verification) pass")
+        ms_ar, mean_ar, _ = timed(Z.PASS_AR_INFILL, max(10, args.steps // 2), 3)
+        result["ar_infill_pass"] = {"steps_per_s": 1e3 / ms_ar, "slot_attn_us": mean_ar[0] * 1e3}
+        del sets
+        torch.cuda.empty_cache()
+        result["layout_attention"] = layout_attention(dev, max(5, args.steps // 10))
+
+    if not args.no_cpu_baseline:
+        log("timing the float64 CPU oracle (reference baseline)")
+        result["cpu_baseline"] = cpu_baseline(wl, x, c)
+    print(json.dumps(result), flush=True)
+
+
+def layout_attention(dev, K):
+    """Causal attention over the reordered training layout (B=8, 16/8 heads,
+    N=4096 = 128 slots x 32 tokens, every slot AR_INFILL with earlier slots
+    visible), through zarya_slot_attn with cross_slot = CAUSAL and no prefix."""
+    import numpy as np
+    import torch
+
+    import workloads as W
+    import paper_2609_19868_amd as Z
+
+    wl = W.WORKLOADS["layout"]
+    log("generating layout-attention inputs")
+    x = W.attention_inputs(wl)
+    xd = {k: torch.from_numpy(np.ascontiguousarray(v).view(np.int16)).view(torch.bfloat16).to(dev) for k, v in x.items()}
+    out = torch.empty_like(xd["q"])
+    run = lambda: Z.slot_attn(xd["q"], None, None, xd["k_slot"], xd["v_slot"], wl.n_slots, wl.slot_len,
+                              pass_=Z.PASS_AR_INFILL, cross_slot=Z.CROSS_SLOT_CAUSAL, out=out, want_lse=False)
+    for _ in range(2):
+        run()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(K):
+        run()
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / K
+    N = wl.T
+    flops = 4.0 * wl.batch * wl.n_q_heads * wl.head_dim * (N * (N + 1) / 2)  # causal QK^T + PV
+    tf = flops / (ms * 1e-3) / 1e12
+    return {"us": ms * 1e3, "tflops": tf, "frac_bf16_peak": tf / PEAK_BF16_TFLOPS,
+            "shape": "B=8 Hq/Hkv=16/8 D=128 N=4096 (128 slots x 32), causal"}
+
+
+if __name__ == "__main__":
+    main()

@@ -167,3 +167,43 @@ def test_full_size_sampled(name):
             last = np.arange(wl.n_slots) * wl.slot_len + wl.slot_len - 1
             assert np.abs(Og[:, :, last] - last_diff[0][:, :, last]).max() <= 1e-2
             assert np.abs(Lg[:, :, last] - last_diff[1][:, :, last]).max() <= 1e-4
+
+
+def _layout_case(wl, dev, variant, picks=None):
+    """Training-layout attention: P = 0, every slot sees the earlier slots.
+    Paper-literal reading: causal in physical order (every slot AR_INFILL).
+    Variant: the masked slots (after the clean ones) are bidirectional inside."""
+    x = W.attention_inputs(wl)
+    xd = {k: to_dev(v, wl.dtype, dev) for k, v in x.items()}
+    order, masked_phys = W.training_layout(wl)
+    sp = masked_phys.astype(np.uint8) * 0 + 1  # all AR_INFILL
+    if variant:
+        sp = np.where(masked_phys, 0, 1).astype(np.uint8)  # masked slots DIFFUSION
+    say(f"layout attention N={wl.T} variant={variant}")
+    out, lse = Z.slot_attn(xd["q"], None, None, xd["k_slot"], xd["v_slot"], wl.n_slots, wl.slot_len,
+                           pass_=Z.PASS_AR_INFILL, cross_slot=Z.CROSS_SLOT_CAUSAL,
+                           slot_pass=torch.from_numpy(sp).to(dev))
+    torch.cuda.synchronize()
+    Og, Lg = to_f64(out), to_f64(lse)
+    G = wl.n_q_heads // wl.n_kv_heads
+    pairs = picks if picks is not None else [(b, h) for b in range(wl.batch) for h in range(wl.n_q_heads)]
+    for b, h in pairs:
+        g = h // G
+        sub = wl.replace(batch=1, n_q_heads=1, n_kv_heads=1)
+        xf = {k: W.as_f64(x[k][b:b + 1, (h if k == "q" else g):(h if k == "q" else g) + 1], "bf16")
+              for k in ("q", "k_cache", "v_cache", "k_slot", "v_slot")}
+        O, L = _oracle(xf, sub, oracle.PASS_AR_INFILL, cross=oracle.CROSS_SLOT_CAUSAL, slot_pass=sp[b:b + 1])
+        check_attn(Og[b:b + 1, h:h + 1], Lg[b:b + 1, h:h + 1], O, L, "bf16", f"layout b={b} h={h} variant={variant}")
+
+
+@pytest.mark.parametrize("variant", [False, True], ids=["causal", "masked_bidirectional"])
+def test_training_layout_small(variant):
+    dev = require_gpu()
+    wl = W.WORKLOADS["layout"].replace(batch=2, n_q_heads=4, n_kv_heads=2, n_slots=16, slot_len=32, seed=81)
+    _layout_case(wl, dev, variant)
+
+
+def test_training_layout_full_size_sampled():
+    dev = require_gpu()
+    wl = W.WORKLOADS["layout"]
+    _layout_case(wl, dev, False, picks=[(0, 0), (7, 15)])
