@@ -57,7 +57,8 @@ def build(verbose: bool = False) -> str:
     with cf.ThreadPoolExecutor(max_workers=min(8, len(sources))) as ex:
         outs = list(ex.map(lambda so: _run([hipcc, *HIPCC_FLAGS, "-c", so[0], "-o", so[1]]), zip(sources, objs)))
     tmp = LIB_PATH + ".tmp"
-    _run([hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs])
+    # -z defs: a kernel whose host launch stub was not emitted fails the link here
+    _run([hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", "-Wl,-z,defs", "-o", tmp, *objs])
     os.replace(tmp, LIB_PATH)
     if verbose:
         for o in outs:

@@ -128,17 +128,20 @@ zarya_status check_conf_desc(const zarya_conf_desc* d) {
     return fail(ZARYA_ERR_UNSUPPORTED, "f32 hidden size %d exceeds 8192", d->hidden);
   if (d->dtype == ZARYA_DTYPE_F32 && d->n_rows > 65535)
     return fail(ZARYA_ERR_UNSUPPORTED, "f32 path supports at most 65535 rows");
+  if ((int64_t)d->n_rows * d->hidden * 2 >= ((int64_t)1 << 32))
+    return fail(ZARYA_ERR_UNSUPPORTED, "hidden states of %lld bytes exceed 4 GiB",
+                (long long)d->n_rows * d->hidden * 2);
   return ZARYA_OK;
 }
 
 ConfPlan plan_conf(const zarya_conf_desc* d) {
   ConfPlan pl{};
   if (d->dtype == ZARYA_DTYPE_BF16) {
-    pl.n_rt = (d->n_rows + kConfTileRows - 1) / kConfTileRows;
+    pl.n_rt = (d->n_rows + conf_tile_rows() - 1) / conf_tile_rows();
     const int nblk = (d->vocab + 31) / 32;
-    // one workgroup per compute unit: split the vocabulary so that
-    // row tiles x vocabulary groups is about 256
-    pl.n_vg = std::max(1, std::min(nblk, 256 / pl.n_rt));
+    // split the vocabulary so that row tiles x vocabulary groups reaches the
+    // workgroup count the kernel is tuned for
+    pl.n_vg = std::max(1, std::min(nblk, conf_target_workgroups() / pl.n_rt));
   } else {
     pl.n_rt = 1;
     pl.n_vg = std::max(1, std::min(64, d->vocab / 2048));

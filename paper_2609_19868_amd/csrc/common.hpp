@@ -39,6 +39,54 @@ __device__ __forceinline__ f32x16 mfma32x32x16(const bf16x8& a, const bf16x8& b,
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+typedef __attribute__((address_space(3))) void* lds_ptr;
+
+// Direct global -> LDS load of 16 bytes per lane: lane l's bytes land at
+// lds_base + 16*l (lds_base must be wave-uniform).  A plain (non-template)
+// function: the builtin called straight from a kernel template stops clang
+// from emitting that template's host-side launch stub.
+__device__ __forceinline__ void dma16(const void* src, void* lds_base) {
+  __builtin_amdgcn_global_load_lds(src, (lds_ptr)lds_base, 16, 0, 0);
+}
+
+// Wait until at most N vector-memory operations of this wave are in flight
+// (direct global->LDS loads count until their data is in LDS).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Workgroup barrier that orders LDS accesses (this wave's LDS operations are
+// complete) without waiting for the wave's outstanding global->LDS prefetches,
+// which the __syncthreads() fence would drain.
+__device__ __forceinline__ void block_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// LDS byte address of a pointer into a __shared__ array.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)(lds_ptr)p; }
+
+// 16-byte LDS read issued exactly where it stands in the program (the
+// compiler sinks plain LDS loads next to their use, which exposes the LDS
+// latency in MFMA loops).  The result is only valid after a matching
+// lds_wait<N>() that also names the fragment.
+template <int OFF>
+__device__ __forceinline__ bf16x8 lds_read_b128(uint32_t addr) {
+  bf16x8 r;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF));
+  return r;
+}
+
+// Wait until at most N LDS operations of this wave are outstanding.
+template <int N>
+__device__ __forceinline__ void lds_wait() {
+  asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Order a use of `x` after the preceding lds_wait (volatile asm statements
+// keep their relative order; the tie makes x's consumers depend on it).
+__device__ __forceinline__ void lds_tie(bf16x8& x) { asm volatile("" : "+v"(x)); }
+
 // Work-item index for workgroup `bid` of a grid of `8 * per_xcd` workgroups.
 // Workgroups are dispatched round-robin over the 8 XCDs (bid % 8); this gives
 // each XCD a contiguous run of work items so that neighbouring items (which

@@ -42,8 +42,8 @@ struct AttnParams32 {
   int rows_total;
 };
 
-// LM-head confidence.  Partials are per (vocab group, row), in log2 units:
-// m = max of logit*log2(e), s = sum of 2^(x - m), idx = lowest id at the max.
+// LM-head confidence.  Partials are per (vocab group, row): m = max logit,
+// s = sum of exp(logit - m), idx = lowest id at the max.
 struct ConfParams {
   const void* hidden;   // [M, H]
   const void* w_vocab;  // [V, H]
@@ -85,8 +85,10 @@ struct SelectParams {
 
 constexpr int kAttnKeysPerTile = 64;
 constexpr int kAttnRowsPerBlock = 128;
-constexpr int kConfTileV = 256;
-constexpr int kConfTileRows = 256;
+// hidden rows per workgroup tile and workgroup count the bf16 confidence
+// kernel is tuned for (the vocabulary is split to reach that count)
+int conf_tile_rows();
+int conf_target_workgroups();
 
 hipError_t launch_slot_attn_bf16(const AttnParams& p, int head_dim, hipStream_t stream);
 hipError_t launch_slot_attn_f32(const AttnParams32& p, int head_dim, hipStream_t stream);

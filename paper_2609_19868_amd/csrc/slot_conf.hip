@@ -7,15 +7,17 @@
 // row, the largest softmax probability, its token id (lowest on ties), the
 // log-sum-exp and optionally the probability of a given target id.
 //
-// bf16 design: a workgroup owns a 256-row tile of `hidden` and a contiguous
-// vocabulary range, walked in 256-wide tiles.  The product is computed
-// transposed, logits^T = W h^T, with v_mfma_f32_32x32x16_bf16 (each of the 8
-// waves owns 128 vocab x 64 rows), so every lane holds values of a single
+// bf16 design: a workgroup owns a tile of rows of `hidden` (256 by default)
+// and a contiguous vocabulary range, walked in 256-wide tiles.  The product is
+// computed transposed, logits^T = W h^T, with v_mfma_f32_32x32x16_bf16 (each
+// wave owns 128 vocab ids x 64 rows), so every lane holds values of a single
 // row and the per-row reduction runs inside the lane.  After each vocab tile
-// the epilogue folds the tile into running (max, sum 2^(x-max), argmax)
-// statistics in the log2 domain; at the end of the range the two lane halves
-// and the two vocab halves are combined and one partial per (row, range) is
-// written.  Operands go through double-buffered, XOR-swizzled LDS tiles.
+// the epilogue folds the tile into running (max, sum exp(x - max), argmax)
+// statistics; at the end of the range the two lane halves and the two vocab
+// halves are combined and one partial per (row, range) is written.
+// Operands are streamed into a ring of XOR-swizzled LDS stages with direct
+// global->LDS loads (no register staging), one workgroup barrier per stage;
+// the MFMA operand fragments are read from LDS one k-step ahead of their use.
 // Workgroups that share a vocabulary range are mapped to the same XCD so each
 // W tile is fetched from HBM once and reused from that XCD's L2.
 #include <limits.h>
@@ -27,19 +29,15 @@ namespace zarya {
 
 namespace {
 
-constexpr int BV = kConfTileV;     // vocab entries per tile
-constexpr int BR = kConfTileRows;  // hidden rows per tile
-constexpr int BK = 32;             // contraction depth per LDS stage
-constexpr int ROWB = BK * 2;       // bytes per LDS row
+constexpr int BV = 256;  // vocab entries per tile
 
-__device__ __forceinline__ int coff(int row, int ch) { return row * ROWB + ((ch ^ ((row >> 2) & 3)) << 4); }
-
-// Merge two (max, sum, argmax) statistics in the log2 domain.  On equal maxima
-// the lower id wins, which keeps the result independent of the merge order.
+// Merge two (max logit, sum exp(logit - max), argmax) statistics.  On equal
+// maxima the lower id wins, which keeps the result independent of the merge
+// order.
 __device__ __forceinline__ void stat_merge(float& m, float& s, int& idx, float m2, float s2, int idx2) {
   const float mn = fmaxf(m, m2);
-  const float sa = s == 0.f ? 0.f : s * fast_exp2(m - mn);
-  const float sb = s2 == 0.f ? 0.f : s2 * fast_exp2(m2 - mn);
+  const float sa = s == 0.f ? 0.f : s * fast_exp2((m - mn) * kLog2e);
+  const float sb = s2 == 0.f ? 0.f : s2 * fast_exp2((m2 - mn) * kLog2e);
   int in;
   if (m2 > m) {
     in = idx2;
@@ -53,10 +51,47 @@ __device__ __forceinline__ void stat_merge(float& m, float& s, int& idx, float m
   idx = in;
 }
 
+// XOR swizzle of the 16-byte column of row r in a [rows][BK] bf16 LDS tile:
+// keeps the 32 rows read by one MFMA operand load (and the rows one direct
+// load writes) on distinct LDS banks.
+template <int BK>
+__device__ __forceinline__ int cswz(int r) {
+  if constexpr (BK == 64) {
+    return (r >> 1) & 7;
+  } else {
+    return (r >> 2) & 3;
+  }
+}
+
+template <int BK>
+__device__ __forceinline__ int coff(int r, int ch) {
+  return r * (BK * 2) + ((ch ^ cswz<BK>(r)) << 4);
+}
+
 }  // namespace
 
-__global__ __launch_bounds__(512) void slot_conf_bf16_kernel(ConfParams p) {
-  __shared__ __attribute__((aligned(16))) uint8_t lds[2][2][BV * ROWB];  // [buf][W | hidden]
+// One workgroup: NW waves as a 2 (vocab) x NW/2 (rows) grid over a
+// 256-vocab x BR-row tile; each wave owns 128 vocab ids x 2*BR/NW rows.
+// BK: contraction depth per stage; NS: stages in the LDS ring (prefetch
+// distance NS - 1).  Partials are written per (vocabulary group, row).
+template <int NW, int BR, int BK, int NS>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) void slot_conf_bf16_kernel(
+    ConfParams p) {
+  constexpr int ATB = BV * BK * 2;    // bytes of the W tile of one stage
+  constexpr int BTB = BR * BK * 2;    // bytes of the hidden tile of one stage
+  constexpr int CPA = ATB / 1024 / NW;  // 1 KB direct-load chunks per wave: W
+  constexpr int CPB = BTB / 1024 / NW;  // ... hidden
+  constexpr int LPW = CPA + CPB;        // direct loads per wave per stage
+  constexpr int LPR = BK / 8;           // 16-byte columns per row
+  constexpr int RPC = 1024 / (BK * 2);  // rows per 1 KB chunk
+  constexpr int IB = 4;                 // 32-wide vocab blocks per wave
+  constexpr int WROWS = 2 * BR / NW;    // rows per wave
+  constexpr int JB = WROWS / 32;        // 32-wide row blocks per wave
+  constexpr int NKS = BK / 16;          // MFMA k-steps per stage
+  static_assert(CPA * NW * 1024 == ATB && CPB * NW * 1024 == BTB, "chunks must divide over the waves");
+  static_assert(JB * 32 == WROWS, "rows per wave must be a multiple of 32");
+  __shared__ __attribute__((aligned(16))) uint8_t lds[NS][ATB + BTB];  // per stage: [W tile | hidden tile]
+
   const int w = xcd_work_index(blockIdx.x, p.per_xcd, p.n_items);
   if (w < 0) return;
   const int rt = w % p.n_rt, vg = w / p.n_rt;
@@ -70,140 +105,261 @@ __global__ __launch_bounds__(512) void slot_conf_bf16_kernel(ConfParams p) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n = lane & 31, hh = lane >> 5;
-  const int wv = wave & 1, wr = wave >> 1;  // vocab half, row quarter
+  const int wv = wave & 1, wr = wave >> 1;  // vocab half, row slice
+  const int rbase = wr * WROWS;
 
   const uint16_t* W = static_cast<const uint16_t*>(p.w_vocab);
   const uint16_t* X = static_cast<const uint16_t*>(p.hidden);
 
-  uint4 areg[2], breg[2];
-  auto load = [&](int vt, int kk) {
+  // Direct-to-LDS staging: load j of a wave fills 1 KB chunk c = NW*j + wave
+  // of an operand tile; lane l lands at byte 16*l of it, i.e. row RPC*c + l/LPR
+  // and physical column l%LPR, and fetches the logical column the swizzle puts
+  // there.  Rows past the vocabulary range or the row count are clamped to a
+  // valid row (their results are masked or never stored); columns past H are
+  // clamped and zeroed in LDS before use.
+  const int nks = (H + BK - 1) / BK;
+  const int n_st = n_vt * nks;
+  const bool k_ragged = (H % BK) != 0;
+  const int lcol = lane % LPR, lrow = lane / LPR;
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);  // wave index in a scalar register
+  // Per-lane byte offsets of the bytes this lane fetches, relative to a
+  // wave-uniform base that only moves with the stage: fixed for the whole
+  // hidden tile, and for a vocab tile of W (recomputed when the tile changes,
+  // which also applies the row clamp of the last tile).
+  int a_r[CPA], a_col[CPA];
+  uint32_t a_off[CPA], b_off[CPB];
+  int b_col[CPB];
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int c = j * 512 + tid;
-      const int r = c >> 2, ch = c & 3;
-      const int k = kk + ch * 8;
-      const int vid = v_lo + vt * BV + r;
-      const int hr = row0 + r;
-      areg[j] = (vid < v_hi && k < H) ? *reinterpret_cast<const uint4*>(W + (size_t)vid * H + k) : make_uint4(0, 0, 0, 0);
-      breg[j] = (hr < p.M && k < H) ? *reinterpret_cast<const uint4*>(X + (size_t)hr * H + k) : make_uint4(0, 0, 0, 0);
+  for (int j = 0; j < CPA; ++j) {
+    a_r[j] = RPC * (NW * j + wave_u) + lrow;
+    a_col[j] = 8 * (lcol ^ cswz<BK>(a_r[j]));
+  }
+#pragma unroll
+  for (int j = 0; j < CPB; ++j) {
+    const int r = RPC * (NW * j + wave_u) + lrow;
+    b_col[j] = 8 * (lcol ^ cswz<BK>(r));
+    b_off[j] = (uint32_t)((size_t)min(row0 + r, p.M - 1) * H + b_col[j]) * 2u;
+  }
+  auto set_vocab_tile = [&](int vt) {
+    const int vb = v_lo + vt * BV;
+#pragma unroll
+    for (int j = 0; j < CPA; ++j)
+      a_off[j] = (uint32_t)((size_t)(min(vb + a_r[j], p.V - 1) - vb) * H + a_col[j]) * 2u;
+  };
+  int cur_vt = -1;
+  auto issue = [&](int st, int buf) {
+    const int vt = st / nks, kk = (st - vt * nks) * BK;
+    if (vt != cur_vt) {
+      set_vocab_tile(vt);
+      cur_vt = vt;
+    }
+    const char* wbase = reinterpret_cast<const char*>(W + (size_t)(v_lo + vt * BV) * H + kk);
+    const char* xbase = reinterpret_cast<const char*>(X + kk);
+    uint8_t* dst = &lds[buf][wave_u * 1024];
+    if (!k_ragged || kk + BK <= H) {
+#pragma unroll
+      for (int j = 0; j < CPA; ++j) dma16(wbase + a_off[j], dst + NW * j * 1024);
+#pragma unroll
+      for (int j = 0; j < CPB; ++j) dma16(xbase + b_off[j], dst + ATB + NW * j * 1024);
+    } else {  // the last, partial k-stage: clamp the columns past H (zeroed before use)
+#pragma unroll
+      for (int j = 0; j < CPA; ++j) {
+        const int dk = min(kk + a_col[j], H - 8) - (kk + a_col[j]);
+        dma16(wbase + a_off[j] + 2 * dk, dst + NW * j * 1024);
+      }
+#pragma unroll
+      for (int j = 0; j < CPB; ++j) {
+        const int dk = min(kk + b_col[j], H - 8) - (kk + b_col[j]);
+        dma16(xbase + b_off[j] + 2 * dk, dst + ATB + NW * j * 1024);
+      }
     }
   };
-  auto store = [&](int buf) {
+  auto zero_k_tail = [&](int st, int buf) {
+    const int kk = (st % nks) * BK;
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int c = j * 512 + tid;
-      const int r = c >> 2, ch = c & 3;
-      *reinterpret_cast<uint4*>(&lds[buf][0][coff(r, ch)]) = areg[j];
-      *reinterpret_cast<uint4*>(&lds[buf][1][coff(r, ch)]) = breg[j];
-    }
+    for (int j = 0; j < CPA; ++j)
+      if (kk + a_col[j] >= H) *reinterpret_cast<uint4*>(&lds[buf][(NW * j + wave) * 1024 + lane * 16]) = make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int j = 0; j < CPB; ++j)
+      if (kk + b_col[j] >= H)
+        *reinterpret_cast<uint4*>(&lds[buf][ATB + (NW * j + wave) * 1024 + lane * 16]) = make_uint4(0, 0, 0, 0);
   };
 
-  f32x16 acc[4][2];
+  f32x16 acc[IB][JB];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < IB; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
-  float m_run[2], s_run[2];
-  int i_run[2];
+    for (int j = 0; j < JB; ++j) acc[i][j] = f32x16{};
+  float m_run[JB], s_run[JB];
+  int i_run[JB];
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
+  for (int j = 0; j < JB; ++j) {
     m_run[j] = kNegBig;
     s_run[j] = 0.f;
     i_run[j] = INT_MAX;
   }
 
-  const int nks = (H + BK - 1) / BK;
-  const int n_st = n_vt * nks;
-  load(0, 0);
-  store(0);
-  __syncthreads();
+  for (int st = 0; st < NS - 1 && st < n_st; ++st) issue(st, st);
 
   for (int i = 0; i < n_st; ++i) {
-    const int buf = i & 1;
-    if (i + 1 < n_st) load((i + 1) / nks, ((i + 1) % nks) * BK);
+    const int buf = i % NS;
+    // stage i has landed once at most `ahead` later stages (LPW loads each) are in flight
+    const int ahead = min(n_st - 1, i + NS - 2) - i;
+    if constexpr (NS >= 4) {
+      if (ahead >= 2) {
+        wait_vmcnt<2 * LPW>();
+      } else if (ahead == 1) {
+        wait_vmcnt<LPW>();
+      } else {
+        wait_vmcnt<0>();
+      }
+    } else if constexpr (NS == 3) {
+      if (ahead >= 1) {
+        wait_vmcnt<LPW>();
+      } else {
+        wait_vmcnt<0>();
+      }
+    } else {
+      wait_vmcnt<0>();
+    }
+    if (k_ragged && (i % nks) == nks - 1) zero_k_tail(i, buf);
+    block_barrier();
+    // the buffer consumed in the previous iteration is free for stage i+NS-1
+    if (i + NS - 1 < n_st) issue(i + NS - 1, (i + NS - 1) % NS);
+
     const int vt = i / nks;
     const int vbase = v_lo + vt * BV + wv * 128;  // first vocab id of this wave's half
     const bool active = vbase < v_hi;
     if (active) {
-      const uint8_t* la = lds[buf][0];
-      const uint8_t* lb = lds[buf][1];
+      // Operand fragments are double-buffered across k-steps: the LDS reads of
+      // step ks+1 are issued before the MFMAs of step ks, which wait only for
+      // their own reads.  The swizzle of every row a lane reads depends on the
+      // lane alone, so one base address per step plus immediate offsets
+      // address all fragments of that step.
+      const uint32_t sbase = lds_addr(lds[buf]);
+      bf16x8 a[2][IB], bfr[2][JB];
+      auto frag_load = [&](int ks, int sl) {
+        const uint32_t col = ((2 * ks + hh) ^ cswz<BK>(n)) << 4;
+        const uint32_t pa = sbase + (wv * 128 + n) * (BK * 2) + col;
+        const uint32_t pb = sbase + ATB + (rbase + n) * (BK * 2) + col;
+        a[sl][0] = lds_read_b128<0 * 32 * BK * 2>(pa);
+        a[sl][1] = lds_read_b128<1 * 32 * BK * 2>(pa);
+        a[sl][2] = lds_read_b128<2 * 32 * BK * 2>(pa);
+        a[sl][3] = lds_read_b128<3 * 32 * BK * 2>(pa);
+        bfr[sl][0] = lds_read_b128<0>(pb);
+        if constexpr (JB > 1) bfr[sl][1] = lds_read_b128<1 * 32 * BK * 2>(pb);
+        if constexpr (JB > 2) bfr[sl][2] = lds_read_b128<2 * 32 * BK * 2>(pb);
+        if constexpr (JB > 3) bfr[sl][3] = lds_read_b128<3 * 32 * BK * 2>(pb);
+      };
+      static_assert(IB == 4 && JB <= 4, "fragment loads are written out for IB = 4, JB <= 4");
+      frag_load(0, 0);
 #pragma unroll
-      for (int ks = 0; ks < BK / 16; ++ks) {
-        bf16x8 a[4], bfr[2];
+      for (int ks = 0; ks < NKS; ++ks) {
+        const int sl = ks & 1;
+        if (ks + 1 < NKS) {
+          frag_load(ks + 1, sl ^ 1);
+          lds_wait<IB + JB>();  // this step's reads are done, the next step's may fly
+        } else {
+          lds_wait<0>();
+        }
 #pragma unroll
-        for (int ib = 0; ib < 4; ++ib)
-          a[ib] = *reinterpret_cast<const bf16x8*>(la + coff(wv * 128 + ib * 32 + n, 2 * ks + hh));
+        for (int ib = 0; ib < IB; ++ib) lds_tie(a[sl][ib]);
 #pragma unroll
-        for (int jb = 0; jb < 2; ++jb)
-          bfr[jb] = *reinterpret_cast<const bf16x8*>(lb + coff(wr * 64 + jb * 32 + n, 2 * ks + hh));
+        for (int jb = 0; jb < JB; ++jb) lds_tie(bfr[sl][jb]);
 #pragma unroll
-        for (int ib = 0; ib < 4; ++ib)
+        for (int ib = 0; ib < IB; ++ib)
 #pragma unroll
-          for (int jb = 0; jb < 2; ++jb) acc[ib][jb] = mfma32x32x16(a[ib], bfr[jb], acc[ib][jb]);
+          for (int jb = 0; jb < JB; ++jb) acc[ib][jb] = mfma32x32x16(a[sl][ib], bfr[sl][jb], acc[ib][jb]);
       }
     }
     if (i % nks == nks - 1) {
       if (active) {
-        // fold this vocab tile into the running statistics of the lane's 2 rows;
-        // register v of block ib holds vocab id vbase + 32*ib + 8*(v/4) + 4*hh + v%4.
-        // Ids are visited in increasing order, so a strict '>' keeps the lowest id.
-        const int nvalid = v_hi - vbase;  // ids at local offset >= nvalid are masked
+        // Fold this vocab tile into the running statistics of the lane's rows.
+        // Register v of block ib holds vocab id vbase + 4*hh + c(ib, v) with
+        // the compile-time offset c = 32*ib + 8*(v/4) + v%4.  The argmax is
+        // searched only when the tile raises the running maximum; the lowest
+        // id at the maximum wins (earlier tiles hold lower ids).
+        const int lim = v_hi - vbase - 4 * hh;  // offsets c >= lim are past the range
 #pragma unroll
-        for (int jb = 0; jb < 2; ++jb) {
-          float mt = kNegBig;
-          int it = INT_MAX;
+        for (int jb = 0; jb < JB; ++jb) {
+          float mt = -INFINITY;
+          if (lim >= 128) {
 #pragma unroll
-          for (int ib = 0; ib < 4; ++ib)
+            for (int ib = 0; ib < IB; ++ib) {
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-              const int off = ib * 32 + 8 * (v >> 2) + 4 * hh + (v & 3);
-              const float x = off < nvalid ? acc[ib][jb][v] : -INFINITY;
-              if (x > mt) {
-                mt = x;
-                it = off;
+              for (int v = 0; v < 16; v += 2) mt = fmaxf(mt, fmaxf(acc[ib][jb][v], acc[ib][jb][v + 1]));
+              __builtin_amdgcn_sched_barrier(0);  // keep the epilogue's live ranges short
+            }
+          } else {
+#pragma unroll
+            for (int ib = 0; ib < IB; ++ib)
+#pragma unroll
+              for (int v = 0; v < 16; ++v) {
+                const int c = ib * 32 + 8 * (v >> 2) + (v & 3);
+                mt = fmaxf(mt, c < lim ? acc[ib][jb][v] : -INFINITY);
               }
-            }
-          mt *= kLog2e;
+          }
+          if (mt > m_run[jb]) {
+            int it = 0;
+#pragma unroll
+            for (int ib = IB - 1; ib >= 0; --ib)
+#pragma unroll
+              for (int v = 15; v >= 0; --v) {
+                const int c = ib * 32 + 8 * (v >> 2) + (v & 3);
+                it = (acc[ib][jb][v] == mt && c < lim) ? c : it;
+              }
+            i_run[jb] = vbase + 4 * hh + it;
+          }
           const float mn = fmaxf(m_run[jb], mt);
+          const float mn2 = mn * kLog2e;
           float e = 0.f;
+          if (lim >= 128) {
 #pragma unroll
-          for (int ib = 0; ib < 4; ++ib)
+            for (int ib = 0; ib < IB; ++ib) {
+              float e4[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-              const int off = ib * 32 + 8 * (v >> 2) + 4 * hh + (v & 3);
-              const float pe = fast_exp2(fmaf(acc[ib][jb][v], kLog2e, -mn));
-              e += off < nvalid ? pe : 0.f;
+              for (int v = 0; v < 16; ++v) e4[v & 3] += fast_exp2(fmaf(acc[ib][jb][v], kLog2e, -mn2));
+              e += (e4[0] + e4[1]) + (e4[2] + e4[3]);
+              __builtin_amdgcn_sched_barrier(0);
             }
-          s_run[jb] = s_run[jb] * fast_exp2(m_run[jb] - mn) + e;
-          if (mt > m_run[jb]) i_run[jb] = vbase + it;
+          } else {
+#pragma unroll
+            for (int ib = 0; ib < IB; ++ib)
+#pragma unroll
+              for (int v = 0; v < 16; ++v) {
+                const int c = ib * 32 + 8 * (v >> 2) + (v & 3);
+                const float pe = fast_exp2(fmaf(acc[ib][jb][v], kLog2e, -mn2));
+                e += c < lim ? pe : 0.f;
+              }
+          }
+          s_run[jb] = s_run[jb] * fast_exp2((m_run[jb] - mn) * kLog2e) + e;
           m_run[jb] = mn;
         }
       }
 #pragma unroll
-      for (int ib = 0; ib < 4; ++ib)
+      for (int ib = 0; ib < IB; ++ib)
 #pragma unroll
-        for (int jb = 0; jb < 2; ++jb) acc[ib][jb] = f32x16{};
+        for (int jb = 0; jb < JB; ++jb) acc[ib][jb] = f32x16{};
     }
-    if (i + 1 < n_st) store(buf ^ 1);
-    __syncthreads();
   }
+  block_barrier();  // every wave is done with the stage buffers (reused below)
 
   // combine the lane halves (disjoint vocab ids of the same rows)
 #pragma unroll
-  for (int jb = 0; jb < 2; ++jb) {
+  for (int jb = 0; jb < JB; ++jb) {
     const float m2 = __shfl_xor(m_run[jb], 32);
     const float s2 = __shfl_xor(s_run[jb], 32);
     const int i2 = __shfl_xor(i_run[jb], 32);
     stat_merge(m_run[jb], s_run[jb], i_run[jb], m2, s2, i2);
   }
-  // combine the two vocab halves through LDS (the tiles are no longer needed)
-  float* xm = reinterpret_cast<float*>(&lds[0][0][0]);
-  float* xs = xm + 256;
-  int* xi = reinterpret_cast<int*>(xs + 256);
+  // combine the two vocab halves through LDS
+  float* xm = reinterpret_cast<float*>(&lds[0][0]);
+  float* xs = xm + BR;
+  int* xi = reinterpret_cast<int*>(xs + BR);
   if (wv == 1 && hh == 0) {
 #pragma unroll
-    for (int jb = 0; jb < 2; ++jb) {
-      const int lr = wr * 64 + jb * 32 + n;
+    for (int jb = 0; jb < JB; ++jb) {
+      const int lr = rbase + jb * 32 + n;
       xm[lr] = m_run[jb];
       xs[lr] = s_run[jb];
       xi[lr] = i_run[jb];
@@ -212,8 +368,8 @@ __global__ __launch_bounds__(512) void slot_conf_bf16_kernel(ConfParams p) {
   __syncthreads();
   if (wv == 0 && hh == 0) {
 #pragma unroll
-    for (int jb = 0; jb < 2; ++jb) {
-      const int lr = wr * 64 + jb * 32 + n;
+    for (int jb = 0; jb < JB; ++jb) {
+      const int lr = rbase + jb * 32 + n;
       stat_merge(m_run[jb], s_run[jb], i_run[jb], xm[lr], xs[lr], xi[lr]);
       const int row = row0 + lr;
       if (row < p.M) {
@@ -243,13 +399,12 @@ __global__ __launch_bounds__(256) void slot_conf_f32_kernel(ConfParams p) {
     const float* wr = W + (size_t)v * p.H;
     float z = 0.f;
     for (int k = 0; k < p.H; ++k) z = fmaf(hs[k], wr[k], z);
-    const float x = z * kLog2e;
-    if (x > m) {
-      s = s * fast_exp2(m - x) + 1.f;
-      m = x;
+    if (z > m) {
+      s = s * fast_exp2((m - z) * kLog2e) + 1.f;
+      m = z;
       idx = v;
     } else {
-      s += fast_exp2(x - m);
+      s += fast_exp2((z - m) * kLog2e);
     }
   }
   float* rm = hs + p.H;
@@ -279,7 +434,7 @@ __global__ __launch_bounds__(256) void slot_conf_f32_kernel(ConfParams p) {
 }
 
 // Per row: merge the vocabulary-group partials in a fixed order and finish
-// max_prob = 1 / sum 2^(x - max), lse and the target probability.
+// max_prob = 1 / sum exp(x - max), lse and the target probability.
 __global__ __launch_bounds__(256) void slot_conf_merge_kernel(ConfMergeParams p) {
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
@@ -297,7 +452,7 @@ __global__ __launch_bounds__(256) void slot_conf_merge_kernel(ConfMergeParams p)
     const int i2 = __shfl_xor(idx, off);
     stat_merge(m, s, idx, m2, s2, i2);
   }
-  const float lse2 = m + __log2f(s);
+  const float lse2 = m * kLog2e + __log2f(s);
   float z = 0.f;
   int tgt = -1;
   if (p.target_ids) {
@@ -325,8 +480,31 @@ __global__ __launch_bounds__(256) void slot_conf_merge_kernel(ConfMergeParams p)
   }
 }
 
+// Tile configuration (measured on MI355X over the 0.6B/1.7B/4B LM-head
+// shapes): 8 waves over a 256 x 256 tile, 64-deep stages, two LDS stages
+// (128 KB), one workgroup per compute unit.
+#ifndef ZARYA_CONF_NW
+#define ZARYA_CONF_NW 8
+#endif
+#ifndef ZARYA_CONF_BR
+#define ZARYA_CONF_BR 256
+#endif
+#ifndef ZARYA_CONF_BK
+#define ZARYA_CONF_BK 64
+#endif
+#ifndef ZARYA_CONF_NS
+#define ZARYA_CONF_NS 2
+#endif
+#ifndef ZARYA_CONF_WGS
+#define ZARYA_CONF_WGS 256  // workgroups to aim for: one per compute unit
+#endif
+
+int conf_tile_rows() { return ZARYA_CONF_BR; }
+int conf_target_workgroups() { return ZARYA_CONF_WGS; }
+
 hipError_t launch_slot_conf_bf16(const ConfParams& p, hipStream_t stream) {
-  hipLaunchKernelGGL(slot_conf_bf16_kernel, dim3(8 * p.per_xcd), dim3(512), 0, stream, p);
+  slot_conf_bf16_kernel<ZARYA_CONF_NW, ZARYA_CONF_BR, ZARYA_CONF_BK, ZARYA_CONF_NS>
+      <<<dim3(8 * p.per_xcd), dim3(ZARYA_CONF_NW * 64), 0, stream>>>(p);
   return hipGetLastError();
 }
 
