@@ -88,10 +88,11 @@ AttnPlan plan_attn(const zarya_slot_attn_desc* d) {
     if (d->prefix_splits > 0) {
       ns = d->prefix_splits;
     } else {
-      // aim for about two workgroups per compute unit, with at least two key
-      // tiles per split so the partial traffic stays small
+      // aim for about one workgroup per compute unit (measured best on the
+      // 0.6B/1.7B/4B shapes), with at least two key tiles per split so the
+      // partial traffic stays small
       const int64_t base = (int64_t)d->batch * d->n_kv_heads * pl.n_rb;
-      const int64_t want = (512 + base - 1) / base;
+      const int64_t want = (256 + base - 1) / base;
       ns = (int)std::min<int64_t>(16, std::max<int64_t>(1, want));
       ns = std::max(1, std::min(ns, pl.n_prefix_tiles / 2));
     }

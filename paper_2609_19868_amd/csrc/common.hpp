@@ -77,6 +77,16 @@ __device__ __forceinline__ bf16x8 lds_read_b128(uint32_t addr) {
   return r;
 }
 
+// Transposing 8-byte LDS read (ds_read_b64_tr_b16), issued where it stands;
+// valid after a matching lds_wait<N>() / lds_tie.  In each 16-lane group,
+// output lane i, element j comes from input lane 4*j + i/4, element i%4.
+template <int OFF>
+__device__ __forceinline__ v4i16 lds_read_tr16_b64(uint32_t addr) {
+  v4i16 r;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF));
+  return r;
+}
+
 // Wait until at most N LDS operations of this wave are outstanding.
 template <int N>
 __device__ __forceinline__ void lds_wait() {
@@ -86,6 +96,15 @@ __device__ __forceinline__ void lds_wait() {
 // Order a use of `x` after the preceding lds_wait (volatile asm statements
 // keep their relative order; the tie makes x's consumers depend on it).
 __device__ __forceinline__ void lds_tie(bf16x8& x) { asm volatile("" : "+v"(x)); }
+__device__ __forceinline__ void lds_tie(v4i16& x) { asm volatile("" : "+v"(x)); }
+
+// Two floats -> packed bf16x2 (low half = a) with the hardware conversion
+// (round to nearest even).
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack_bf16x2_hw(float a, float b) {
+  bf16x2_t v = {(__bf16)a, (__bf16)b};
+  return __builtin_bit_cast(uint32_t, v);
+}
 
 // Work-item index for workgroup `bid` of a grid of `8 * per_xcd` workgroups.
 // Workgroups are dispatched round-robin over the 8 XCDs (bid % 8); this gives

@@ -29,13 +29,22 @@
 
 namespace zarya {
 
+#ifndef ZARYA_ATTN_NS
+#define ZARYA_ATTN_NS 2  // LDS stages of the bf16 kernel (2 x 32 KB: two workgroups per CU)
+#endif
+#ifndef ZARYA_ATTN_WPE
+#define ZARYA_ATTN_WPE 2  // waves per SIMD the register budget is sized for
+#endif
+
 namespace {
 
-constexpr int KT = 64;      // keys per tile
-constexpr int NWAVE = 4;    // waves per workgroup
+constexpr int KT = 64;          // keys per tile
+constexpr int NWAVE = 4;        // waves per workgroup
 constexpr int RB = NWAVE * 32;  // query rows per workgroup
 
-// XOR swizzle of the 16-byte chunk index of LDS row `kr`.
+// XOR swizzle of the 16-byte chunk index of LDS row `kr` (D = 128: 16 chunks
+// per row; D = 64: 8).  Keeps the 32 rows of one K-fragment read and the 4
+// rows of one transposing V read on distinct banks.
 template <int D>
 __device__ __forceinline__ int swz(int kr) {
   if constexpr (D == 128) {
@@ -45,21 +54,21 @@ __device__ __forceinline__ int swz(int kr) {
   }
 }
 
-template <int D>
-__device__ __forceinline__ int lds_off(int kr, int chunk) {
-  return kr * (D * 2) + ((chunk ^ swz<D>(kr)) << 4);
-}
-
 }  // namespace
 
-template <int D>
-__global__ __launch_bounds__(256) void slot_attn_bf16_kernel(AttnParams p) {
-  constexpr int NCH = D / 8;           // 16-byte chunks per key row
-  constexpr int TILEB = KT * D * 2;    // bytes of one K (or V) tile
-  constexpr int NLD = TILEB / (256 * 16);  // 16-byte loads per thread per tile
-  constexpr int NDB = D / 32;          // 32-wide blocks of the head dim
-  constexpr int NKS = D / 16;          // k-steps of the QK^T contraction
-  __shared__ __attribute__((aligned(16))) uint8_t lds[2][2][TILEB];
+// NS: LDS stages (prefetch distance NS - 1 tiles).
+template <int D, int NS>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(ZARYA_ATTN_WPE))) void slot_attn_bf16_kernel(AttnParams p) {
+  constexpr int ROWB = D * 2;           // bytes per key row
+  constexpr int TILEB = KT * ROWB;      // bytes of one K (or V) tile
+  constexpr int CPW = TILEB / 1024 / NWAVE;  // 1 KB direct loads per wave per tile (K; same for V)
+  constexpr int LPR = ROWB / 16;        // lanes per row in a direct load
+  constexpr int RPC = 1024 / ROWB;      // rows per 1 KB chunk
+  constexpr int NDB = D / 32;           // 32-wide blocks of the head dim
+  constexpr int NKS = D / 16;           // k-steps of the QK^T contraction
+  constexpr int LPT = 2 * CPW;          // direct loads per wave per tile
+  static_assert(CPW * NWAVE * 1024 == TILEB, "tile must split into 1 KB chunks per wave");
+  __shared__ __attribute__((aligned(16))) uint8_t lds[NS][2][TILEB];
 
   const int w = xcd_work_index(blockIdx.x, p.per_xcd, p.n_items);
   if (w < 0) return;
@@ -70,9 +79,10 @@ __global__ __launch_bounds__(256) void slot_attn_bf16_kernel(AttnParams p) {
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
   const int n = lane & 31, hh = lane >> 5;
 
-  // ---- this lane's query row and its visible range of draft-token keys
+  // ---- this lane's query row and its visible range [vis_lo, vis_hi) of draft-token keys
   const int row = rb * RB + wave * 32 + n;  // row of the GQA group, [0, G*T)
   const bool row_ok = row < p.R;
   int vis_lo = 0, vis_hi = 0;
@@ -105,10 +115,9 @@ __global__ __launch_bounds__(256) void slot_attn_bf16_kernel(AttnParams p) {
   }
   const int nt = n_pre + n_slot;
 
-  const size_t cache_base = (size_t)bg * p.C * D;
-  const size_t slot_base = (size_t)bg * p.T * D;
-
-  // ---- Q fragments (B operand of S^T = K Q^T), kept in registers
+  // ---- Q fragments (B operand of S^T = K Q^T), kept in registers; loaded
+  // and waited for before the direct-load pipeline starts so that the
+  // pipeline's counted waits see only its own loads
   bf16x8 qf[NKS];
   {
     const uint4* qrow = reinterpret_cast<const uint4*>(p.q + ((size_t)bg * p.R + (row_ok ? row : 0)) * D);
@@ -117,151 +126,221 @@ __global__ __launch_bounds__(256) void slot_attn_bf16_kernel(AttnParams p) {
       uint4 v = row_ok ? qrow[2 * ks + hh] : make_uint4(0, 0, 0, 0);
       qf[ks] = __builtin_bit_cast(bf16x8, v);
     }
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) lds_tie(qf[ks]);
+    wait_vmcnt<0>();
   }
 
-  uint4 kreg[NLD], vreg[NLD];
-  auto load_tile = [&](int i) {
-    const uint16_t *kp, *vp;
-    int valid;
+  // ---- direct-to-LDS staging of K and V tiles: load j of a wave fills 1 KB
+  // chunk c = 4*j + wave (RPC rows); lane l lands at row RPC*c + l/LPR,
+  // physical 16-byte column l%LPR and fetches the logical column the swizzle
+  // puts there.  Rows past the valid keys are clamped to the last valid row
+  // (their scores are masked, so they contribute exact zeros).
+  int my_r[CPW];
+  uint32_t my_off[CPW];
+#pragma unroll
+  for (int j = 0; j < CPW; ++j) {
+    my_r[j] = RPC * (NWAVE * j + wave_u) + lane / LPR;
+    my_off[j] = (uint32_t)(my_r[j] * ROWB + (((lane % LPR) ^ swz<D>(my_r[j])) << 4));
+  }
+  const char* kc = reinterpret_cast<const char*>(p.k_cache + (size_t)bg * p.C * D);
+  const char* vc = reinterpret_cast<const char*>(p.v_cache + (size_t)bg * p.C * D);
+  const char* ks_ = reinterpret_cast<const char*>(p.k_slot + (size_t)bg * p.T * D);
+  const char* vs_ = reinterpret_cast<const char*>(p.v_slot + (size_t)bg * p.T * D);
+  auto issue = [&](int i, int buf) {
+    const char *kp, *vp;
+    int key0, valid;
     if (i < n_pre) {
-      const int key0 = (pre_begin + i) * KT;
-      kp = p.k_cache + cache_base + (size_t)key0 * D;
-      vp = p.v_cache + cache_base + (size_t)key0 * D;
-      valid = min(KT, p.P - key0);
+      key0 = (pre_begin + i) * KT;
+      kp = kc;
+      vp = vc;
+      valid = p.P - key0;
     } else {
-      const int key0 = slot_lo + (i - n_pre) * KT;
-      kp = p.k_slot + slot_base + (size_t)key0 * D;
-      vp = p.v_slot + slot_base + (size_t)key0 * D;
-      valid = min(KT, p.T - key0);
+      key0 = slot_lo + (i - n_pre) * KT;
+      kp = ks_;
+      vp = vs_;
+      valid = p.T - key0;
     }
+    kp += (size_t)key0 * ROWB;
+    vp += (size_t)key0 * ROWB;
+    uint8_t* kd = &lds[buf][0][wave_u * 1024];
+    uint8_t* vd = &lds[buf][1][wave_u * 1024];
+    if (valid >= KT) {
 #pragma unroll
-    for (int j = 0; j < NLD; ++j) {
-      const int c = j * 256 + tid;
-      const int kr = c / NCH, ch = c % NCH;
-      if (kr < valid) {
-        kreg[j] = reinterpret_cast<const uint4*>(kp + (size_t)kr * D)[ch];
-        vreg[j] = reinterpret_cast<const uint4*>(vp + (size_t)kr * D)[ch];
-      } else {  // rows past the end: zeros, so masked probabilities multiply finite values
-        kreg[j] = make_uint4(0, 0, 0, 0);
-        vreg[j] = make_uint4(0, 0, 0, 0);
+      for (int j = 0; j < CPW; ++j) {
+        dma16(kp + my_off[j], kd + NWAVE * j * 1024);
+        dma16(vp + my_off[j], vd + NWAVE * j * 1024);
       }
-    }
-  };
-  auto store_tile = [&](int buf) {
+    } else {
 #pragma unroll
-    for (int j = 0; j < NLD; ++j) {
-      const int c = j * 256 + tid;
-      const int kr = c / NCH, ch = c % NCH;
-      *reinterpret_cast<uint4*>(&lds[buf][0][lds_off<D>(kr, ch)]) = kreg[j];
-      *reinterpret_cast<uint4*>(&lds[buf][1][lds_off<D>(kr, ch)]) = vreg[j];
+      for (int j = 0; j < CPW; ++j) {
+        const int dr = min(my_r[j], valid - 1) - my_r[j];  // <= 0: clamp to the last valid row
+        dma16(kp + my_off[j] + dr * ROWB, kd + NWAVE * j * 1024);
+        dma16(vp + my_off[j] + dr * ROWB, vd + NWAVE * j * 1024);
+      }
     }
   };
 
   f32x16 oacc[NDB];
 #pragma unroll
   for (int db = 0; db < NDB; ++db) oacc[db] = f32x16{};
-  float m_run = kNegBig, l_run = 0.f;
+  float m_run = kNegBig, l_run = 0.f;  // running max of raw scores; sum of 2^(scaled score - scaled max)
+  const float c2 = p.scale_log2;
 
-  if (nt > 0) {
-    load_tile(0);
-    store_tile(0);
+  // lane-dependent parts of the LDS fragment addresses (the swizzle of every
+  // row a lane reads depends on the lane only)
+  const uint32_t lds0 = lds_addr(&lds[0][0][0]);
+  uint32_t k_col[NKS];
+#pragma unroll
+  for (int ks = 0; ks < NKS; ++ks) k_col[ks] = n * ROWB + (((2 * ks + hh) ^ swz<D>(n)) << 4);
+  const int q16 = lane >> 4, rr = lane & 15;
+  const int vrow = 4 * hh + (rr >> 2);  // first key row of this lane's transposing reads (+16*st, +8)
+  uint32_t v_col[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) {
+    const int d = db * 32 + (q16 & 1) * 16 + 4 * (rr & 3);
+    v_col[db] = vrow * ROWB + (((d >> 3) ^ swz<D>(vrow)) << 4) + (d & 7) * 2;
   }
-  __syncthreads();
+
+  for (int st = 0; st < NS - 1 && st < nt; ++st) issue(st, st);
 
   for (int i = 0; i < nt; ++i) {
-    const int buf = i & 1;
-    if (i + 1 < nt) load_tile(i + 1);
-    const uint8_t* kl = lds[buf][0];
-    const uint8_t* vl = lds[buf][1];
+    const int buf = i % NS;
+    const int ahead = min(nt - 1, i + NS - 2) - i;  // later tiles whose loads may still fly
+    if constexpr (NS >= 4) {
+      if (ahead >= 2) {
+        wait_vmcnt<2 * LPT>();
+      } else if (ahead == 1) {
+        wait_vmcnt<LPT>();
+      } else {
+        wait_vmcnt<0>();
+      }
+    } else if constexpr (NS == 3) {
+      if (ahead >= 1) {
+        wait_vmcnt<LPT>();
+      } else {
+        wait_vmcnt<0>();
+      }
+    } else {
+      wait_vmcnt<0>();
+    }
+    block_barrier();
+    if (i + NS - 1 < nt) issue(i + NS - 1, (i + NS - 1) % NS);
 
-    // S^T for two 32-key blocks: reg v of block kb is key kb*32 + 8*(v/4) + 4*hh + v%4
-    f32x16 sacc[2];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      sacc[kb] = f32x16{};
+    const uint32_t kb_addr = lds0 + buf * (2 * TILEB);
+    const uint32_t vb_addr = kb_addr + TILEB;
+
+    // ---- S^T = K Q^T for two 32-key blocks; register v of block kb holds
+    // key kb*32 + 8*(v/4) + 4*hh + v%4 of the tile.  K fragments are read
+    // one k-step ahead of their MFMAs.
+    f32x16 sacc[2] = {f32x16{}, f32x16{}};
+    {
+      bf16x8 kf[2][2];
+      kf[0][0] = lds_read_b128<0>(kb_addr + k_col[0]);
+      kf[0][1] = lds_read_b128<32 * ROWB>(kb_addr + k_col[0]);
 #pragma unroll
       for (int ks = 0; ks < NKS; ++ks) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(kl + lds_off<D>(kb * 32 + n, 2 * ks + hh));
-        sacc[kb] = mfma32x32x16(a, qf[ks], sacc[kb]);
+        const int sl = ks & 1;
+        if (ks + 1 < NKS) {
+          kf[sl ^ 1][0] = lds_read_b128<0>(kb_addr + k_col[ks + 1]);
+          kf[sl ^ 1][1] = lds_read_b128<32 * ROWB>(kb_addr + k_col[ks + 1]);
+          lds_wait<2>();
+        } else {
+          lds_wait<0>();
+        }
+        lds_tie(kf[sl][0]);
+        lds_tie(kf[sl][1]);
+        sacc[0] = mfma32x32x16(kf[sl][0], qf[ks], sacc[0]);
+        sacc[1] = mfma32x32x16(kf[sl][1], qf[ks], sacc[1]);
       }
     }
 
-    // scale into the log2 domain and mask
-    float sv[2][16];
-    const bool is_slot = i >= n_pre;
-    int key0, lim_lo, lim_n;
-    if (!is_slot) {
-      key0 = (pre_begin + i) * KT;
-      lim_lo = key0;
-      lim_n = p.P - key0;  // keys [key0, P) valid
-    } else {
-      key0 = slot_lo + (i - n_pre) * KT;
-      lim_lo = vis_lo;
-      lim_n = vis_hi - vis_lo;
-    }
-    float mt = kNegBig;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int key = key0 + kb * 32 + 8 * (v >> 2) + 4 * hh + (v & 3);
-        const bool vis = (unsigned)(key - lim_lo) < (unsigned)lim_n;
-        const float x = vis ? sacc[kb][v] * p.scale_log2 : -INFINITY;
-        sv[kb][v] = x;
-        mt = fmaxf(mt, x);
-      }
-    }
-    mt = fmaxf(mt, __shfl_xor(mt, 32));
-    const float m_new = fmaxf(m_run, mt);
-    const float alpha = fast_exp2(m_run - m_new);
-    m_run = m_new;
-    float psum = 0.f;
-    // B operand of PV step st, slot j = accumulator register 8*(st%2) + j of key
-    // block st/2; packed two bf16 per dword and bit-cast as whole vectors
-    uint32_t pk[4][4];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-      for (int v = 0; v < 16; v += 2) {
-        const float e0 = fast_exp2(sv[kb][v] - m_new);
-        const float e1 = fast_exp2(sv[kb][v + 1] - m_new);
-        psum += e0 + e1;
-        pk[2 * kb + (v >> 3)][(v & 7) >> 1] = pack_bf16x2(e0, e1);
-      }
-    }
-    bf16x8 pb[4];
-#pragma unroll
-    for (int st = 0; st < 4; ++st) pb[st] = __builtin_bit_cast(bf16x8, make_uint4(pk[st][0], pk[st][1], pk[st][2], pk[st][3]));
-    l_run = l_run * alpha + psum;
-#pragma unroll
-    for (int db = 0; db < NDB; ++db)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) oacc[db][v] *= alpha;
-
-    // O^T += V^T P^T.  Step st covers keys 16*st + 4*hh + {0..3} (slots 0-3)
-    // and 16*st + 8 + 4*hh + {0..3} (slots 4-7); lane-group row rr = lane%16
-    // reads 4 d-values of key (.. + rr/4) for the transposing load.
-    const int q16 = lane >> 4, rr = lane & 15;
-    const int dgrp = q16 & 1;
+    // ---- V^T fragments of the first PV step, issued before the softmax
+    v4i16 vf[2][NDB][2];
 #pragma unroll
     for (int db = 0; db < NDB; ++db) {
-      const int d = db * 32 + dgrp * 16 + 4 * (rr & 3);
-      const int chunk = d >> 3, half = (d & 7) * 2;
-#pragma unroll
-      for (int st = 0; st < 4; ++st) {
-        const int k0 = 16 * st + 4 * hh + (rr >> 2);
-        const int k1 = k0 + 8;
-        v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(vl + lds_off<D>(k0, chunk) + half));
-        v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(vl + lds_off<D>(k1, chunk) + half));
-        const uint2 l2 = __builtin_bit_cast(uint2, lo);
-        const uint2 h2 = __builtin_bit_cast(uint2, hi);
-        const bf16x8 a = __builtin_bit_cast(bf16x8, make_uint4(l2.x, l2.y, h2.x, h2.y));
-        oacc[db] = mfma32x32x16(a, pb[st], oacc[db]);
-      }
+      vf[0][db][0] = lds_read_tr16_b64<0>(vb_addr + v_col[db]);
+      vf[0][db][1] = lds_read_tr16_b64<8 * ROWB>(vb_addr + v_col[db]);
     }
 
-    if (i + 1 < nt) store_tile(buf ^ 1);
-    __syncthreads();
+    // ---- online softmax; masks only on tiles that need them
+    const bool is_slot = i >= n_pre;
+    const int key0 = is_slot ? slot_lo + (i - n_pre) * KT : (pre_begin + i) * KT;
+    const bool full = !is_slot && key0 + KT <= p.P;
+    const int lim_lo = is_slot ? vis_lo : key0;
+    const int lim_n = is_slot ? vis_hi - vis_lo : p.P - key0;
+    float mt = -INFINITY;
+    if (!full) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int key = key0 + kb * 32 + 8 * (v >> 2) + 4 * hh + (v & 3);
+          if ((unsigned)(key - lim_lo) >= (unsigned)lim_n) sacc[kb][v] = -INFINITY;
+        }
+    }
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int v = 0; v < 16; v += 2) mt = fmaxf(mt, fmaxf(sacc[kb][v], sacc[kb][v + 1]));
+    mt = fmaxf(mt, __shfl_xor(mt, 32));
+    const float m_new = fmaxf(m_run, mt);
+    if (__any(m_new > m_run)) {  // the running maximum moved for some row: rescale
+      const float alpha = fast_exp2((m_run - m_new) * c2);
+      l_run *= alpha;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) oacc[db][v] *= alpha;
+      m_run = m_new;
+    }
+    const float mc = m_run * c2;
+    float ps[4] = {0.f, 0.f, 0.f, 0.f};
+    bf16x8 pb[4];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        uint32_t pk[4];
+#pragma unroll
+        for (int j = 0; j < 8; j += 2) {
+          const int v = half * 8 + j;
+          const float e0 = fast_exp2(fmaf(sacc[kb][v], c2, -mc));
+          const float e1 = fast_exp2(fmaf(sacc[kb][v + 1], c2, -mc));
+          ps[j >> 1] += e0 + e1;
+          pk[j >> 1] = pack_bf16x2_hw(e0, e1);
+        }
+        // B operand of PV step 2*kb + half: slot j = accumulator register 8*half + j
+        pb[2 * kb + half] = __builtin_bit_cast(bf16x8, make_uint4(pk[0], pk[1], pk[2], pk[3]));
+      }
+    l_run += (ps[0] + ps[1]) + (ps[2] + ps[3]);
+
+    // ---- O^T += V^T P^T.  Step st covers keys 16*st + 4*hh + {0..3} (slots
+    // 0-3) and 16*st + 8 + 4*hh + {0..3} (slots 4-7); V^T fragments are read
+    // one step ahead with the transposing LDS read.
+#pragma unroll
+    for (int stp = 0; stp < 4; ++stp) {
+      const int sl = stp & 1;
+      if (stp + 1 < 4) {
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) {
+          vf[sl ^ 1][db][0] = lds_read_tr16_b64<0>(vb_addr + v_col[db] + 16 * (stp + 1) * ROWB);
+          vf[sl ^ 1][db][1] = lds_read_tr16_b64<8 * ROWB>(vb_addr + v_col[db] + 16 * (stp + 1) * ROWB);
+        }
+        lds_wait<2 * NDB>();
+      } else {
+        lds_wait<0>();
+      }
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        lds_tie(vf[sl][db][0]);
+        lds_tie(vf[sl][db][1]);
+        const uint2 l2 = __builtin_bit_cast(uint2, vf[sl][db][0]);
+        const uint2 h2 = __builtin_bit_cast(uint2, vf[sl][db][1]);
+        const bf16x8 a = __builtin_bit_cast(bf16x8, make_uint4(l2.x, l2.y, h2.x, h2.y));
+        oacc[db] = mfma32x32x16(a, pb[stp], oacc[db]);
+      }
+    }
   }
 
   // ---- finalize: combine the two lane halves' partial sums
@@ -269,6 +348,7 @@ __global__ __launch_bounds__(256) void slot_attn_bf16_kernel(AttnParams p) {
   if (!row_ok) return;
   const size_t grow = (size_t)bg * p.R + row;  // row of the [B*Hq*T] output
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+  const float lse2 = m_run * c2 + __log2f(l_tot);  // log2 units
   if (p.n_split == 1) {
     uint16_t* orow = p.out + grow * D;
 #pragma unroll
@@ -277,11 +357,11 @@ __global__ __launch_bounds__(256) void slot_attn_bf16_kernel(AttnParams p) {
       for (int u = 0; u < 4; ++u) {
         const int d = db * 32 + 8 * u + 4 * hh;
         uint2 pk;
-        pk.x = pack_bf16x2(oacc[db][4 * u] * inv, oacc[db][4 * u + 1] * inv);
-        pk.y = pack_bf16x2(oacc[db][4 * u + 2] * inv, oacc[db][4 * u + 3] * inv);
+        pk.x = pack_bf16x2_hw(oacc[db][4 * u] * inv, oacc[db][4 * u + 1] * inv);
+        pk.y = pack_bf16x2_hw(oacc[db][4 * u + 2] * inv, oacc[db][4 * u + 3] * inv);
         *reinterpret_cast<uint2*>(orow + d) = pk;
       }
-    if (p.lse && hh == 0) p.lse[grow] = (m_run + __log2f(l_tot)) * kLn2;
+    if (p.lse && hh == 0) p.lse[grow] = lse2 * kLn2;
   } else {
     float* orow = p.part_o + ((size_t)split * p.rows_total + grow) * D;
 #pragma unroll
@@ -293,7 +373,7 @@ __global__ __launch_bounds__(256) void slot_attn_bf16_kernel(AttnParams p) {
                                 oacc[db][4 * u + 3] * inv);
         *reinterpret_cast<float4*>(orow + d) = o4;
       }
-    if (hh == 0) p.part_lse[(size_t)split * p.rows_total + grow] = l_tot > 0.f ? m_run + __log2f(l_tot) : -INFINITY;
+    if (hh == 0) p.part_lse[(size_t)split * p.rows_total + grow] = l_tot > 0.f ? lse2 : -INFINITY;
   }
 }
 
@@ -323,7 +403,7 @@ __global__ __launch_bounds__(256) void slot_attn_merge_kernel(const float* __res
   const float inv = 1.f / wsum;
   uint16_t* orow = out + (size_t)row * D + lane * PER;
   if constexpr (PER == 2) {
-    *reinterpret_cast<uint32_t*>(orow) = pack_bf16x2(acc[0] * inv, acc[1] * inv);
+    *reinterpret_cast<uint32_t*>(orow) = pack_bf16x2_hw(acc[0] * inv, acc[1] * inv);
   } else {
     orow[0] = f32_to_bf16(acc[0] * inv);
   }
@@ -381,9 +461,9 @@ __global__ __launch_bounds__(64) void slot_attn_f32_kernel(AttnParams32 p) {
 hipError_t launch_slot_attn_bf16(const AttnParams& p, int head_dim, hipStream_t stream) {
   const int grid = 8 * p.per_xcd;
   if (head_dim == 128) {
-    hipLaunchKernelGGL(slot_attn_bf16_kernel<128>, dim3(grid), dim3(256), 0, stream, p);
+    slot_attn_bf16_kernel<128, ZARYA_ATTN_NS><<<dim3(grid), dim3(256), 0, stream>>>(p);
   } else {
-    hipLaunchKernelGGL(slot_attn_bf16_kernel<64>, dim3(grid), dim3(256), 0, stream, p);
+    slot_attn_bf16_kernel<64, ZARYA_ATTN_NS><<<dim3(grid), dim3(256), 0, stream>>>(p);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.n_split == 1) return e;
