@@ -109,6 +109,8 @@ def main():
     ap.add_argument("--workload", default="qwen0.6b", choices=["qwen0.6b", "qwen1.7b", "qwen4b"])
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the CPU oracle leg")
     ap.add_argument("--no-extras", action="store_true", help="skip the AR_INFILL and layout-attention timings")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device-to-device copy (scale reference for HBM byte counters)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -124,6 +126,9 @@ def main():
     import paper_2609_19868_amd as Z
 
     dev = torch.device("cuda:0")
+    if args.copy_calibration:
+        copy_calibration(dev, args.steps)
+        return
     wl = W.WORKLOADS[args.workload]
     B, Hq, Hkv, D, P, S, L, H, V = (wl.batch, wl.n_q_heads, wl.n_kv_heads, wl.head_dim, wl.prefix_len, wl.n_slots,
                                     wl.slot_len, wl.hidden, wl.vocab)
@@ -262,6 +267,27 @@ def main():
         log("timing the float64 CPU oracle (reference baseline)")
         result["cpu_baseline"] = cpu_baseline(wl, x, c)
     print(json.dumps(result), flush=True)
+
+
+def copy_calibration(dev, K):
+    """A plain copy of known size: read 1 GiB, write 1 GiB, K times.  Under
+    rocprofv3 --pmc its FETCH_SIZE / WRITE_SIZE per dispatch give the factor
+    between the counters' reading and the bytes actually moved."""
+    import torch
+
+    n = 1 << 30
+    src = torch.randint(0, 255, (n,), dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(K):
+        dst.copy_(src)
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / K
+    print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "us": ms * 1e3,
+                      "gbps": 2 * n / (ms * 1e-3) / 1e9}), flush=True)
 
 
 def layout_attention(dev, K):

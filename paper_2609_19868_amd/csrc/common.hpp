@@ -98,6 +98,15 @@ __device__ __forceinline__ void lds_wait() {
 __device__ __forceinline__ void lds_tie(bf16x8& x) { asm volatile("" : "+v"(x)); }
 __device__ __forceinline__ void lds_tie(v4i16& x) { asm volatile("" : "+v"(x)); }
 
+// max(a, b, c) in one v_max3_f32.  fmaxf() of values the compiler cannot
+// prove quiet (MFMA results, say) costs an extra canonicalising max per
+// operand; the operands here are finite.
+__device__ __forceinline__ float max3f(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
 // Two floats -> packed bf16x2 (low half = a) with the hardware conversion
 // (round to nearest even).
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));

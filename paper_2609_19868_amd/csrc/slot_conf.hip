@@ -31,6 +31,7 @@ namespace {
 
 constexpr int BV = 256;  // vocab entries per tile
 
+
 // Merge two (max logit, sum exp(logit - max), argmax) statistics.  On equal
 // maxima the lower id wins, which keeps the result independent of the merge
 // order.
@@ -72,16 +73,17 @@ __device__ __forceinline__ int coff(int r, int ch) {
 
 // One workgroup: NW waves as a 2 (vocab) x NW/2 (rows) grid over a
 // 256-vocab x BR-row tile; each wave owns 128 vocab ids x 2*BR/NW rows.
-// BK: contraction depth per stage; NS: stages in the LDS ring (prefetch
-// distance NS - 1).  Partials are written per (vocabulary group, row).
-template <int NW, int BR, int BK, int NS>
+// BK: contraction depth per stage.  The W tile streams from HBM through a
+// ring of NSW LDS buffers (prefetch distance NSW - 1 stages), the hidden tile
+// (re-read for every vocab tile, so served from L2) through a ring of NSX.
+// Partials are written per (vocabulary group, row).
+template <int NW, int BR, int BK, int NSW, int NSX>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) void slot_conf_bf16_kernel(
     ConfParams p) {
   constexpr int ATB = BV * BK * 2;    // bytes of the W tile of one stage
   constexpr int BTB = BR * BK * 2;    // bytes of the hidden tile of one stage
   constexpr int CPA = ATB / 1024 / NW;  // 1 KB direct-load chunks per wave: W
   constexpr int CPB = BTB / 1024 / NW;  // ... hidden
-  constexpr int LPW = CPA + CPB;        // direct loads per wave per stage
   constexpr int LPR = BK / 8;           // 16-byte columns per row
   constexpr int RPC = 1024 / (BK * 2);  // rows per 1 KB chunk
   constexpr int IB = 4;                 // 32-wide vocab blocks per wave
@@ -90,7 +92,10 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
   constexpr int NKS = BK / 16;          // MFMA k-steps per stage
   static_assert(CPA * NW * 1024 == ATB && CPB * NW * 1024 == BTB, "chunks must divide over the waves");
   static_assert(JB * 32 == WROWS, "rows per wave must be a multiple of 32");
-  __shared__ __attribute__((aligned(16))) uint8_t lds[NS][ATB + BTB];  // per stage: [W tile | hidden tile]
+  static_assert(NSX == 2 && (NSW == 2 || NSW == 3), "the load waits below are written for these ring depths");
+  static_assert(NSW * ATB + NSX * BTB <= 160 * 1024, "LDS rings exceed 160 KB");
+  __shared__ __attribute__((aligned(16))) uint8_t lds_w[NSW][ATB];
+  __shared__ __attribute__((aligned(16))) uint8_t lds_x[NSX][BTB];
 
   const int w = xcd_work_index(blockIdx.x, p.per_xcd, p.n_items);
   if (w < 0) return;
@@ -140,56 +145,57 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
     b_col[j] = 8 * (lcol ^ cswz<BK>(r));
     b_off[j] = (uint32_t)((size_t)min(row0 + r, p.M - 1) * H + b_col[j]) * 2u;
   }
-  auto set_vocab_tile = [&](int vt) {
-    const int vb = v_lo + vt * BV;
-#pragma unroll
-    for (int j = 0; j < CPA; ++j)
-      a_off[j] = (uint32_t)((size_t)(min(vb + a_r[j], p.V - 1) - vb) * H + a_col[j]) * 2u;
-  };
   int cur_vt = -1;
-  auto issue = [&](int st, int buf) {
+  auto issue_w = [&](int st) {
     const int vt = st / nks, kk = (st - vt * nks) * BK;
+    const int vb = v_lo + vt * BV;
     if (vt != cur_vt) {
-      set_vocab_tile(vt);
+#pragma unroll
+      for (int j = 0; j < CPA; ++j)
+        a_off[j] = (uint32_t)((size_t)(min(vb + a_r[j], p.V - 1) - vb) * H + a_col[j]) * 2u;
       cur_vt = vt;
     }
-    const char* wbase = reinterpret_cast<const char*>(W + (size_t)(v_lo + vt * BV) * H + kk);
-    const char* xbase = reinterpret_cast<const char*>(X + kk);
-    uint8_t* dst = &lds[buf][wave_u * 1024];
+    const char* base = reinterpret_cast<const char*>(W + (size_t)vb * H + kk);
+    uint8_t* dst = &lds_w[st % NSW][wave_u * 1024];
     if (!k_ragged || kk + BK <= H) {
 #pragma unroll
-      for (int j = 0; j < CPA; ++j) dma16(wbase + a_off[j], dst + NW * j * 1024);
-#pragma unroll
-      for (int j = 0; j < CPB; ++j) dma16(xbase + b_off[j], dst + ATB + NW * j * 1024);
+      for (int j = 0; j < CPA; ++j) dma16(base + a_off[j], dst + NW * j * 1024);
     } else {  // the last, partial k-stage: clamp the columns past H (zeroed before use)
 #pragma unroll
       for (int j = 0; j < CPA; ++j) {
         const int dk = min(kk + a_col[j], H - 8) - (kk + a_col[j]);
-        dma16(wbase + a_off[j] + 2 * dk, dst + NW * j * 1024);
-      }
-#pragma unroll
-      for (int j = 0; j < CPB; ++j) {
-        const int dk = min(kk + b_col[j], H - 8) - (kk + b_col[j]);
-        dma16(xbase + b_off[j] + 2 * dk, dst + ATB + NW * j * 1024);
+        dma16(base + a_off[j] + 2 * dk, dst + NW * j * 1024);
       }
     }
   };
-  auto zero_k_tail = [&](int st, int buf) {
+  auto issue_x = [&](int st) {
+    const int kk = (st % nks) * BK;
+    const char* base = reinterpret_cast<const char*>(X + kk);
+    uint8_t* dst = &lds_x[st % NSX][wave_u * 1024];
+    if (!k_ragged || kk + BK <= H) {
+#pragma unroll
+      for (int j = 0; j < CPB; ++j) dma16(base + b_off[j], dst + NW * j * 1024);
+    } else {
+#pragma unroll
+      for (int j = 0; j < CPB; ++j) {
+        const int dk = min(kk + b_col[j], H - 8) - (kk + b_col[j]);
+        dma16(base + b_off[j] + 2 * dk, dst + NW * j * 1024);
+      }
+    }
+  };
+  auto zero_k_tail = [&](int st) {
     const int kk = (st % nks) * BK;
 #pragma unroll
     for (int j = 0; j < CPA; ++j)
-      if (kk + a_col[j] >= H) *reinterpret_cast<uint4*>(&lds[buf][(NW * j + wave) * 1024 + lane * 16]) = make_uint4(0, 0, 0, 0);
+      if (kk + a_col[j] >= H)
+        *reinterpret_cast<uint4*>(&lds_w[st % NSW][(NW * j + wave) * 1024 + lane * 16]) = make_uint4(0, 0, 0, 0);
 #pragma unroll
     for (int j = 0; j < CPB; ++j)
       if (kk + b_col[j] >= H)
-        *reinterpret_cast<uint4*>(&lds[buf][ATB + (NW * j + wave) * 1024 + lane * 16]) = make_uint4(0, 0, 0, 0);
+        *reinterpret_cast<uint4*>(&lds_x[st % NSX][(NW * j + wave) * 1024 + lane * 16]) = make_uint4(0, 0, 0, 0);
   };
 
-  f32x16 acc[IB][JB];
-#pragma unroll
-  for (int i = 0; i < IB; ++i)
-#pragma unroll
-    for (int j = 0; j < JB; ++j) acc[i][j] = f32x16{};
+  f32x16 acc[IB][JB];  // set by the first k-step of every vocab tile
   float m_run[JB], s_run[JB];
   int i_run[JB];
 #pragma unroll
@@ -199,49 +205,44 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
     i_run[j] = INT_MAX;
   }
 
-  for (int st = 0; st < NS - 1 && st < n_st; ++st) issue(st, st);
+  // Load order: iteration i issues the hidden tile of stage i+NSX-1, then the
+  // W tile of stage i+NSW-1; the prologue issues what iterations before 0
+  // would have.  Loads complete in issue order, so when the hidden tile of
+  // stage i has landed so has its W tile, and with NSW = 3 only the W tile of
+  // stage i+1 (CPA loads) may still be in flight.
+  for (int j = -(NSW - 1); j < 0; ++j) {
+    if (j + NSX - 1 >= 0 && j + NSX - 1 < n_st) issue_x(j + NSX - 1);
+    if (j + NSW - 1 < n_st) issue_w(j + NSW - 1);
+  }
 
   for (int i = 0; i < n_st; ++i) {
-    const int buf = i % NS;
-    // stage i has landed once at most `ahead` later stages (LPW loads each) are in flight
-    const int ahead = min(n_st - 1, i + NS - 2) - i;
-    if constexpr (NS >= 4) {
-      if (ahead >= 2) {
-        wait_vmcnt<2 * LPW>();
-      } else if (ahead == 1) {
-        wait_vmcnt<LPW>();
-      } else {
-        wait_vmcnt<0>();
-      }
-    } else if constexpr (NS == 3) {
-      if (ahead >= 1) {
-        wait_vmcnt<LPW>();
-      } else {
-        wait_vmcnt<0>();
-      }
+    if (NSW == 3 && i + 1 < n_st) {
+      wait_vmcnt<CPA>();
     } else {
       wait_vmcnt<0>();
     }
-    if (k_ragged && (i % nks) == nks - 1) zero_k_tail(i, buf);
+    if (k_ragged && (i % nks) == nks - 1) zero_k_tail(i);
     block_barrier();
-    // the buffer consumed in the previous iteration is free for stage i+NS-1
-    if (i + NS - 1 < n_st) issue(i + NS - 1, (i + NS - 1) % NS);
+    // the buffers consumed in the previous iteration are free
+    if (i + NSX - 1 < n_st) issue_x(i + NSX - 1);
+    if (i + NSW - 1 < n_st) issue_w(i + NSW - 1);
 
     const int vt = i / nks;
     const int vbase = v_lo + vt * BV + wv * 128;  // first vocab id of this wave's half
     const bool active = vbase < v_hi;
+    const bool fresh = i % nks == 0;
     if (active) {
       // Operand fragments are double-buffered across k-steps: the LDS reads of
       // step ks+1 are issued before the MFMAs of step ks, which wait only for
       // their own reads.  The swizzle of every row a lane reads depends on the
       // lane alone, so one base address per step plus immediate offsets
       // address all fragments of that step.
-      const uint32_t sbase = lds_addr(lds[buf]);
+      const uint32_t wsb = lds_addr(lds_w[i % NSW]), xsb = lds_addr(lds_x[i % NSX]);
       bf16x8 a[2][IB], bfr[2][JB];
       auto frag_load = [&](int ks, int sl) {
         const uint32_t col = ((2 * ks + hh) ^ cswz<BK>(n)) << 4;
-        const uint32_t pa = sbase + (wv * 128 + n) * (BK * 2) + col;
-        const uint32_t pb = sbase + ATB + (rbase + n) * (BK * 2) + col;
+        const uint32_t pa = wsb + (wv * 128 + n) * (BK * 2) + col;
+        const uint32_t pb = xsb + (rbase + n) * (BK * 2) + col;
         a[sl][0] = lds_read_b128<0 * 32 * BK * 2>(pa);
         a[sl][1] = lds_read_b128<1 * 32 * BK * 2>(pa);
         a[sl][2] = lds_read_b128<2 * 32 * BK * 2>(pa);
@@ -266,10 +267,17 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
         for (int ib = 0; ib < IB; ++ib) lds_tie(a[sl][ib]);
 #pragma unroll
         for (int jb = 0; jb < JB; ++jb) lds_tie(bfr[sl][jb]);
+        if (ks == 0 && fresh) {  // the tile's first k-step starts the accumulators from zero
 #pragma unroll
-        for (int ib = 0; ib < IB; ++ib)
+          for (int ib = 0; ib < IB; ++ib)
 #pragma unroll
-          for (int jb = 0; jb < JB; ++jb) acc[ib][jb] = mfma32x32x16(a[sl][ib], bfr[sl][jb], acc[ib][jb]);
+            for (int jb = 0; jb < JB; ++jb) acc[ib][jb] = mfma32x32x16(a[sl][ib], bfr[sl][jb], f32x16{});
+        } else {
+#pragma unroll
+          for (int ib = 0; ib < IB; ++ib)
+#pragma unroll
+            for (int jb = 0; jb < JB; ++jb) acc[ib][jb] = mfma32x32x16(a[sl][ib], bfr[sl][jb], acc[ib][jb]);
+        }
       }
     }
     if (i % nks == nks - 1) {
@@ -283,13 +291,18 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
 #pragma unroll
         for (int jb = 0; jb < JB; ++jb) {
           float mt = -INFINITY;
-          if (lim >= 128) {
+          const bool full = lim >= 128;
+          if (full) {
+            float mq[IB];
 #pragma unroll
             for (int ib = 0; ib < IB; ++ib) {
+              const f32x16& x = acc[ib][jb];
+              float t = max3f(x[0], x[1], x[2]);
 #pragma unroll
-              for (int v = 0; v < 16; v += 2) mt = fmaxf(mt, fmaxf(acc[ib][jb][v], acc[ib][jb][v + 1]));
-              __builtin_amdgcn_sched_barrier(0);  // keep the epilogue's live ranges short
+              for (int v = 3; v < 15; v += 2) t = max3f(t, x[v], x[v + 1]);
+              mq[ib] = max3f(t, x[15], x[15]);
             }
+            mt = max3f(max3f(mq[0], mq[1], mq[2]), mq[3], mq[3]);
           } else {
 #pragma unroll
             for (int ib = 0; ib < IB; ++ib)
@@ -301,19 +314,26 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
           }
           if (mt > m_run[jb]) {
             int it = 0;
+            if (full) {
 #pragma unroll
-            for (int ib = IB - 1; ib >= 0; --ib)
+              for (int ib = IB - 1; ib >= 0; --ib)
 #pragma unroll
-              for (int v = 15; v >= 0; --v) {
-                const int c = ib * 32 + 8 * (v >> 2) + (v & 3);
-                it = (acc[ib][jb][v] == mt && c < lim) ? c : it;
-              }
+                for (int v = 15; v >= 0; --v) it = acc[ib][jb][v] == mt ? ib * 32 + 8 * (v >> 2) + (v & 3) : it;
+            } else {
+#pragma unroll
+              for (int ib = IB - 1; ib >= 0; --ib)
+#pragma unroll
+                for (int v = 15; v >= 0; --v) {
+                  const int c = ib * 32 + 8 * (v >> 2) + (v & 3);
+                  it = (acc[ib][jb][v] == mt && c < lim) ? c : it;
+                }
+            }
             i_run[jb] = vbase + 4 * hh + it;
           }
           const float mn = fmaxf(m_run[jb], mt);
           const float mn2 = mn * kLog2e;
           float e = 0.f;
-          if (lim >= 128) {
+          if (full) {
 #pragma unroll
             for (int ib = 0; ib < IB; ++ib) {
               float e4[4] = {0.f, 0.f, 0.f, 0.f};
@@ -336,10 +356,6 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
           m_run[jb] = mn;
         }
       }
-#pragma unroll
-      for (int ib = 0; ib < IB; ++ib)
-#pragma unroll
-        for (int jb = 0; jb < JB; ++jb) acc[ib][jb] = f32x16{};
     }
   }
   block_barrier();  // every wave is done with the stage buffers (reused below)
@@ -353,7 +369,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
     stat_merge(m_run[jb], s_run[jb], i_run[jb], m2, s2, i2);
   }
   // combine the two vocab halves through LDS
-  float* xm = reinterpret_cast<float*>(&lds[0][0]);
+  float* xm = reinterpret_cast<float*>(&lds_w[0][0]);
   float* xs = xm + BR;
   int* xi = reinterpret_cast<int*>(xs + BR);
   if (wv == 1 && hh == 0) {
@@ -481,8 +497,8 @@ __global__ __launch_bounds__(256) void slot_conf_merge_kernel(ConfMergeParams p)
 }
 
 // Tile configuration (measured on MI355X over the 0.6B/1.7B/4B LM-head
-// shapes): 8 waves over a 256 x 256 tile, 64-deep stages, two LDS stages
-// (128 KB), one workgroup per compute unit.
+// shapes): 8 waves over a 256 x 256 tile, 64-deep stages, three W and two
+// hidden LDS buffers (160 KB), one workgroup per compute unit.
 #ifndef ZARYA_CONF_NW
 #define ZARYA_CONF_NW 8
 #endif
@@ -492,8 +508,11 @@ __global__ __launch_bounds__(256) void slot_conf_merge_kernel(ConfMergeParams p)
 #ifndef ZARYA_CONF_BK
 #define ZARYA_CONF_BK 64
 #endif
-#ifndef ZARYA_CONF_NS
-#define ZARYA_CONF_NS 2
+#ifndef ZARYA_CONF_NSW
+#define ZARYA_CONF_NSW 3
+#endif
+#ifndef ZARYA_CONF_NSX
+#define ZARYA_CONF_NSX 2
 #endif
 #ifndef ZARYA_CONF_WGS
 #define ZARYA_CONF_WGS 256  // workgroups to aim for: one per compute unit
@@ -503,7 +522,7 @@ int conf_tile_rows() { return ZARYA_CONF_BR; }
 int conf_target_workgroups() { return ZARYA_CONF_WGS; }
 
 hipError_t launch_slot_conf_bf16(const ConfParams& p, hipStream_t stream) {
-  slot_conf_bf16_kernel<ZARYA_CONF_NW, ZARYA_CONF_BR, ZARYA_CONF_BK, ZARYA_CONF_NS>
+  slot_conf_bf16_kernel<ZARYA_CONF_NW, ZARYA_CONF_BR, ZARYA_CONF_BK, ZARYA_CONF_NSW, ZARYA_CONF_NSX>
       <<<dim3(8 * p.per_xcd), dim3(ZARYA_CONF_NW * 64), 0, stream>>>(p);
   return hipGetLastError();
 }
