@@ -51,9 +51,9 @@ struct ConfParams {
   int n_vg;        // vocabulary groups (partials per row)
   int n_rt;        // row tiles (bf16 path)
   int per_xcd, n_items;
-  float* part_m;   // [n_vg, M]
-  float* part_s;   // [n_vg, M]
-  int* part_idx;   // [n_vg, M]
+  float* part_m;   // [M, n_vg]
+  float* part_s;   // [M, n_vg]
+  int* part_idx;   // [M, n_vg]
 };
 
 struct ConfMergeParams {

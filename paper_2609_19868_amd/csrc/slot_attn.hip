@@ -269,7 +269,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(ZARYA_ATTN_
     const bool full = !is_slot && key0 + KT <= p.P;
     const int lim_lo = is_slot ? vis_lo : key0;
     const int lim_n = is_slot ? vis_hi - vis_lo : p.P - key0;
-    float mt = -INFINITY;
     if (!full) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
@@ -279,10 +278,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(ZARYA_ATTN_
           if ((unsigned)(key - lim_lo) >= (unsigned)lim_n) sacc[kb][v] = -INFINITY;
         }
     }
+    float mt = max3f(sacc[0][0], sacc[0][1], sacc[1][0]);
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int v = 2; v < 16; v += 2) mt = max3f(mt, sacc[0][v], sacc[0][v + 1]);
 #pragma unroll
-      for (int v = 0; v < 16; v += 2) mt = fmaxf(mt, fmaxf(sacc[kb][v], sacc[kb][v + 1]));
+    for (int v = 1; v < 15; v += 2) mt = max3f(mt, sacc[1][v], sacc[1][v + 1]);
+    mt = max3f(mt, sacc[1][15], sacc[1][15]);
     mt = fmaxf(mt, __shfl_xor(mt, 32));
     const float m_new = fmaxf(m_run, mt);
     if (__any(m_new > m_run)) {  // the running maximum moved for some row: rescale

@@ -71,6 +71,130 @@ __device__ __forceinline__ int coff(int r, int ch) {
 
 }  // namespace
 
+// Fold one vocab tile into the running (max, sum exp(x - max), argmax)
+// statistics of a lane's rows.  Register v of block (ib, jb) holds the logit
+// of vocab id id0 + c(ib, v), c = 32*ib + 8*(v/4) + v%4, for the lane's row of
+// row block jb; offsets c >= lim are past the vocabulary range.  The argmax
+// is searched only when the tile raises the running maximum; the lowest id at
+// the maximum wins (earlier tiles hold lower ids).
+template <int JB>
+__device__ __forceinline__ void fold_tile(const f32x16 (&acc)[4][JB], int lim, int id0, float (&m_run)[JB],
+                                          float (&s_run)[JB], int (&i_run)[JB]) {
+  constexpr int IB = 4;
+  const bool full = lim >= 128;
+#pragma unroll
+  for (int jb = 0; jb < JB; ++jb) {
+    float mt = -INFINITY;
+    if (full) {
+      float mq[IB];
+#pragma unroll
+      for (int ib = 0; ib < IB; ++ib) {
+        const f32x16& x = acc[ib][jb];
+        float t = max3f(x[0], x[1], x[2]);
+#pragma unroll
+        for (int v = 3; v < 15; v += 2) t = max3f(t, x[v], x[v + 1]);
+        mq[ib] = max3f(t, x[15], x[15]);
+      }
+      mt = max3f(max3f(mq[0], mq[1], mq[2]), mq[3], mq[3]);
+    } else {
+#pragma unroll
+      for (int ib = 0; ib < IB; ++ib)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int c = ib * 32 + 8 * (v >> 2) + (v & 3);
+          mt = fmaxf(mt, c < lim ? acc[ib][jb][v] : -INFINITY);
+        }
+    }
+    if (mt > m_run[jb]) {
+      int it = 0;
+      if (full) {
+#pragma unroll
+        for (int ib = IB - 1; ib >= 0; --ib)
+#pragma unroll
+          for (int v = 15; v >= 0; --v) it = acc[ib][jb][v] == mt ? ib * 32 + 8 * (v >> 2) + (v & 3) : it;
+      } else {
+#pragma unroll
+        for (int ib = IB - 1; ib >= 0; --ib)
+#pragma unroll
+          for (int v = 15; v >= 0; --v) {
+            const int c = ib * 32 + 8 * (v >> 2) + (v & 3);
+            it = (acc[ib][jb][v] == mt && c < lim) ? c : it;
+          }
+      }
+      i_run[jb] = id0 + it;
+    }
+    const float mn = fmaxf(m_run[jb], mt);
+    const float mn2 = mn * kLog2e;
+    float e = 0.f;
+    if (full) {
+#pragma unroll
+      for (int ib = 0; ib < IB; ++ib) {
+        float e4[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int v = 0; v < 16; ++v) e4[v & 3] += fast_exp2(fmaf(acc[ib][jb][v], kLog2e, -mn2));
+        e += (e4[0] + e4[1]) + (e4[2] + e4[3]);
+        __builtin_amdgcn_sched_barrier(0);  // keep the live ranges short
+      }
+    } else {
+#pragma unroll
+      for (int ib = 0; ib < IB; ++ib)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int c = ib * 32 + 8 * (v >> 2) + (v & 3);
+          const float pe = fast_exp2(fmaf(acc[ib][jb][v], kLog2e, -mn2));
+          e += c < lim ? pe : 0.f;
+        }
+    }
+    s_run[jb] = s_run[jb] * fast_exp2((m_run[jb] - mn) * kLog2e) + e;
+    m_run[jb] = mn;
+  }
+}
+
+// Combine the statistics of a workgroup's rows and write one partial per
+// (vocabulary group, row).  Lanes n and n+32 hold disjoint vocab ids of the
+// same row (merged by a shuffle); the waves of vocab halves 0 and 1 hold the
+// same rows (merged through `scratch`, 12 bytes per row).  Ends with a
+// workgroup barrier; `scratch` must be free of pending reads.
+template <int JB, int BR>
+__device__ __forceinline__ void store_partials(const ConfParams& p, int vg, int row0, int rbase, int wv, int hh, int n,
+                                               float (&m_run)[JB], float (&s_run)[JB], int (&i_run)[JB],
+                                               uint8_t* scratch) {
+#pragma unroll
+  for (int jb = 0; jb < JB; ++jb) {
+    const float m2 = __shfl_xor(m_run[jb], 32);
+    const float s2 = __shfl_xor(s_run[jb], 32);
+    const int i2 = __shfl_xor(i_run[jb], 32);
+    stat_merge(m_run[jb], s_run[jb], i_run[jb], m2, s2, i2);
+  }
+  float* xm = reinterpret_cast<float*>(scratch);
+  float* xs = xm + BR;
+  int* xi = reinterpret_cast<int*>(xs + BR);
+  if (wv == 1 && hh == 0) {
+#pragma unroll
+    for (int jb = 0; jb < JB; ++jb) {
+      const int lr = rbase + jb * 32 + n;
+      xm[lr] = m_run[jb];
+      xs[lr] = s_run[jb];
+      xi[lr] = i_run[jb];
+    }
+  }
+  __syncthreads();
+  if (wv == 0 && hh == 0) {
+#pragma unroll
+    for (int jb = 0; jb < JB; ++jb) {
+      const int lr = rbase + jb * 32 + n;
+      stat_merge(m_run[jb], s_run[jb], i_run[jb], xm[lr], xs[lr], xi[lr]);
+      const int row = row0 + lr;
+      if (row < p.M) {
+        const size_t o = (size_t)row * p.n_vg + vg;
+        p.part_m[o] = m_run[jb];
+        p.part_s[o] = s_run[jb];
+        p.part_idx[o] = i_run[jb];
+      }
+    }
+  }
+}
+
 // One workgroup: NW waves as a 2 (vocab) x NW/2 (rows) grid over a
 // 256-vocab x BR-row tile; each wave owns 128 vocab ids x 2*BR/NW rows.
 // BK: contraction depth per stage.  The W tile streams from HBM through a
@@ -278,124 +402,16 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
 #pragma unroll
             for (int jb = 0; jb < JB; ++jb) acc[ib][jb] = mfma32x32x16(a[sl][ib], bfr[sl][jb], acc[ib][jb]);
         }
+        // keep this step's MFMAs ahead of the next step's reads and waits
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
     if (i % nks == nks - 1) {
-      if (active) {
-        // Fold this vocab tile into the running statistics of the lane's rows.
-        // Register v of block ib holds vocab id vbase + 4*hh + c(ib, v) with
-        // the compile-time offset c = 32*ib + 8*(v/4) + v%4.  The argmax is
-        // searched only when the tile raises the running maximum; the lowest
-        // id at the maximum wins (earlier tiles hold lower ids).
-        const int lim = v_hi - vbase - 4 * hh;  // offsets c >= lim are past the range
-#pragma unroll
-        for (int jb = 0; jb < JB; ++jb) {
-          float mt = -INFINITY;
-          const bool full = lim >= 128;
-          if (full) {
-            float mq[IB];
-#pragma unroll
-            for (int ib = 0; ib < IB; ++ib) {
-              const f32x16& x = acc[ib][jb];
-              float t = max3f(x[0], x[1], x[2]);
-#pragma unroll
-              for (int v = 3; v < 15; v += 2) t = max3f(t, x[v], x[v + 1]);
-              mq[ib] = max3f(t, x[15], x[15]);
-            }
-            mt = max3f(max3f(mq[0], mq[1], mq[2]), mq[3], mq[3]);
-          } else {
-#pragma unroll
-            for (int ib = 0; ib < IB; ++ib)
-#pragma unroll
-              for (int v = 0; v < 16; ++v) {
-                const int c = ib * 32 + 8 * (v >> 2) + (v & 3);
-                mt = fmaxf(mt, c < lim ? acc[ib][jb][v] : -INFINITY);
-              }
-          }
-          if (mt > m_run[jb]) {
-            int it = 0;
-            if (full) {
-#pragma unroll
-              for (int ib = IB - 1; ib >= 0; --ib)
-#pragma unroll
-                for (int v = 15; v >= 0; --v) it = acc[ib][jb][v] == mt ? ib * 32 + 8 * (v >> 2) + (v & 3) : it;
-            } else {
-#pragma unroll
-              for (int ib = IB - 1; ib >= 0; --ib)
-#pragma unroll
-                for (int v = 15; v >= 0; --v) {
-                  const int c = ib * 32 + 8 * (v >> 2) + (v & 3);
-                  it = (acc[ib][jb][v] == mt && c < lim) ? c : it;
-                }
-            }
-            i_run[jb] = vbase + 4 * hh + it;
-          }
-          const float mn = fmaxf(m_run[jb], mt);
-          const float mn2 = mn * kLog2e;
-          float e = 0.f;
-          if (full) {
-#pragma unroll
-            for (int ib = 0; ib < IB; ++ib) {
-              float e4[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-              for (int v = 0; v < 16; ++v) e4[v & 3] += fast_exp2(fmaf(acc[ib][jb][v], kLog2e, -mn2));
-              e += (e4[0] + e4[1]) + (e4[2] + e4[3]);
-              __builtin_amdgcn_sched_barrier(0);
-            }
-          } else {
-#pragma unroll
-            for (int ib = 0; ib < IB; ++ib)
-#pragma unroll
-              for (int v = 0; v < 16; ++v) {
-                const int c = ib * 32 + 8 * (v >> 2) + (v & 3);
-                const float pe = fast_exp2(fmaf(acc[ib][jb][v], kLog2e, -mn2));
-                e += c < lim ? pe : 0.f;
-              }
-          }
-          s_run[jb] = s_run[jb] * fast_exp2((m_run[jb] - mn) * kLog2e) + e;
-          m_run[jb] = mn;
-        }
-      }
+      if (active) fold_tile<JB>(acc, v_hi - vbase - 4 * hh, vbase + 4 * hh, m_run, s_run, i_run);
     }
   }
   block_barrier();  // every wave is done with the stage buffers (reused below)
-
-  // combine the lane halves (disjoint vocab ids of the same rows)
-#pragma unroll
-  for (int jb = 0; jb < JB; ++jb) {
-    const float m2 = __shfl_xor(m_run[jb], 32);
-    const float s2 = __shfl_xor(s_run[jb], 32);
-    const int i2 = __shfl_xor(i_run[jb], 32);
-    stat_merge(m_run[jb], s_run[jb], i_run[jb], m2, s2, i2);
-  }
-  // combine the two vocab halves through LDS
-  float* xm = reinterpret_cast<float*>(&lds_w[0][0]);
-  float* xs = xm + BR;
-  int* xi = reinterpret_cast<int*>(xs + BR);
-  if (wv == 1 && hh == 0) {
-#pragma unroll
-    for (int jb = 0; jb < JB; ++jb) {
-      const int lr = rbase + jb * 32 + n;
-      xm[lr] = m_run[jb];
-      xs[lr] = s_run[jb];
-      xi[lr] = i_run[jb];
-    }
-  }
-  __syncthreads();
-  if (wv == 0 && hh == 0) {
-#pragma unroll
-    for (int jb = 0; jb < JB; ++jb) {
-      const int lr = rbase + jb * 32 + n;
-      stat_merge(m_run[jb], s_run[jb], i_run[jb], xm[lr], xs[lr], xi[lr]);
-      const int row = row0 + lr;
-      if (row < p.M) {
-        const size_t o = (size_t)vg * p.M + row;
-        p.part_m[o] = m_run[jb];
-        p.part_s[o] = s_run[jb];
-        p.part_idx[o] = i_run[jb];
-      }
-    }
-  }
+  store_partials<JB, BR>(p, vg, row0, rbase, wv, hh, n, m_run, s_run, i_run, &lds_w[0][0]);
 }
 
 // float32 path: one workgroup per (vocabulary group, row); plain FMA dot products.
@@ -442,7 +458,7 @@ __global__ __launch_bounds__(256) void slot_conf_f32_kernel(ConfParams p) {
     __syncthreads();
   }
   if (tid == 0) {
-    const size_t o = (size_t)vg * p.M + row;
+    const size_t o = (size_t)row * p.n_vg + vg;
     p.part_m[o] = rm[0];
     p.part_s[o] = rs[0];
     p.part_idx[o] = ri[0];
@@ -458,7 +474,7 @@ __global__ __launch_bounds__(256) void slot_conf_merge_kernel(ConfMergeParams p)
   float m = kNegBig, s = 0.f;
   int idx = INT_MAX;
   for (int g = lane; g < p.n_vg; g += 64) {
-    const size_t o = (size_t)g * p.M + row;
+    const size_t o = (size_t)row * p.n_vg + g;  // a row's partials are contiguous
     stat_merge(m, s, idx, p.part_m[o], p.part_s[o], p.part_idx[o]);
   }
 #pragma unroll
