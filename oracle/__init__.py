@@ -16,6 +16,9 @@ Language Model with Flexible Training and Dual-Mode Inference"):
   (Sec. 5.2 "probability of its first token", Table 1 tied embedding).
 * ``selection``   -- slot confidence and first-hitting slot selection
   (Sec. 5.2 slot selection, Sec. 6 inference settings).
+* ``verify``      -- token acceptance after the verification pass and the
+  KV-cache append of the accepted tokens (Sec. 5.2 "Verification phase",
+  "KV cache update").
 
 Every function is the plain definition written out in float64 numpy; there is
 no blocking, fusion or reordering beyond what the definition states.
@@ -27,6 +30,7 @@ from .attention import (
     CROSS_SLOT_NONE,
     CROSS_SLOT_CAUSAL,
     visibility,
+    prefix_lengths,
     slot_attention,
     slot_attention_loops,
 )
@@ -39,6 +43,8 @@ from .selection import (
     slot_conf,
     select_slots,
 )
+
+from .verify import ACCEPT_PREFIX, ACCEPT_PER_TOKEN, accept_tokens, kv_append
 
 __all__ = [
     "PASS_DIFFUSION",
@@ -56,4 +62,9 @@ __all__ = [
     "SELECT_TOP_K",
     "slot_conf",
     "select_slots",
+    "prefix_lengths",
+    "ACCEPT_PREFIX",
+    "ACCEPT_PER_TOKEN",
+    "accept_tokens",
+    "kv_append",
 ]

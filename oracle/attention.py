@@ -24,6 +24,11 @@ Paper passages this follows:
   slots to what a token sees, which with every slot in the AR_INFILL pass is
   ordinary causal attention in physical order.
 
+* Sec. 5.2 "KV cache update": accepted tokens are appended to the cache, so
+  after a verification step the batch rows of one call can hold prefixes of
+  different lengths.  ``prefix_len`` is either one length for every row or one
+  length per batch row.
+
 Readings where the paper is silent (each listed in the design notes):
 draft slots do not see each other in the scoring pass (``cross_slot=NONE``);
 query head h uses KV head floor(h / (Hq / Hkv)); the softmax scale is an
@@ -40,6 +45,15 @@ PASS_DIFFUSION = 0
 PASS_AR_INFILL = 1
 CROSS_SLOT_NONE = 0
 CROSS_SLOT_CAUSAL = 1
+
+
+def prefix_lengths(prefix_len, batch):
+    """Per-batch-row prefix lengths from one int or a length-``batch`` sequence."""
+    if np.ndim(prefix_len) == 0:
+        return [int(prefix_len)] * batch
+    pl = [int(x) for x in np.asarray(prefix_len).reshape(-1)]
+    assert len(pl) == batch
+    return pl
 
 
 def _slot_passes(n_slots, pass_, slot_pass):
@@ -91,7 +105,8 @@ def slot_attention(
     """Masked softmax attention, float64.
 
     q       [B, Hq, T, D]       draft-token queries, rows (slot, position)
-    k_cache [B, Hkv, C, D]      prefix keys (first ``prefix_len`` rows valid)
+    k_cache [B, Hkv, C, D]      prefix keys (first ``prefix_len`` rows valid;
+                                ``prefix_len`` is an int or one length per row)
     v_cache [B, Hkv, C, D]
     k_slot  [B, Hkv, T, D]      the draft tokens' own keys
     v_slot  [B, Hkv, T, D]
@@ -106,11 +121,14 @@ def slot_attention(
     Hkv = k_slot.shape[1]
     assert Hq % Hkv == 0 and T == n_slots * slot_len
     G = Hq // Hkv
-    P = int(prefix_len)
+    plens = prefix_lengths(prefix_len, B)
     out = np.empty((B, Hq, T, D), dtype=np.float64)
     lse = np.empty((B, Hq, T), dtype=np.float64)
-    probs = np.empty((B, Hq, T, P + T), dtype=np.float64) if return_probs else None
+    if return_probs:
+        assert len(set(plens)) == 1, "probabilities are returned for one common prefix length"
+    probs = np.empty((B, Hq, T, plens[0] + T), dtype=np.float64) if return_probs else None
     for b in range(B):
+        P = plens[b]
         sp = None if slot_pass is None else np.asarray(slot_pass)[b]
         mask = visibility(P, n_slots, slot_len, pass_, cross_slot, sp)
         for g in range(Hkv):
@@ -147,10 +165,11 @@ def slot_attention_loops(
     B, Hq, T, D = np.shape(q)
     Hkv = np.shape(k_slot)[1]
     G = Hq // Hkv
-    P, L = int(prefix_len), int(slot_len)
+    plens, L = prefix_lengths(prefix_len, B), int(slot_len)
     out = np.zeros((B, Hq, T, D))
     lse = np.zeros((B, Hq, T))
     for b in range(B):
+        P = plens[b]
         for h in range(Hq):
             g = h // G
             for t in range(T):

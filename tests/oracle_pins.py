@@ -239,7 +239,42 @@ def check_bruteforce(attn):
             _close(lse, lseb, tol=1e-12, what=f"brute force LSE case {i}")
 
 
+def check_ragged_rows(attn):
+    """Per-row prefix lengths (Sec. 5.2 KV cache update): each batch row equals
+    the same call made on that row alone with its own prefix length; cache rows
+    past a row's length (random here) never matter."""
+    B, Hq, Hkv, D, S, L, C = 3, 4, 2, 8, 2, 3, 9
+    x = _inputs(60, B, Hq, Hkv, D, C, S, L, C=C)
+    plens = [5, 0, 9]
+    for pass_ in (PASS_DIFFUSION, PASS_AR_INFILL):
+        O, lse = _call(attn, x, plens, S, L, 0.45, pass_)
+        for b, P in enumerate(plens):
+            xb = {k: v[b:b + 1] for k, v in x.items()}
+            Ob, lseb = _call(attn, xb, P, S, L, 0.45, pass_)
+            _close(O[b:b + 1], Ob, tol=1e-13, what=f"ragged row {b} O")
+            _close(lse[b:b + 1], lseb, tol=1e-13, what=f"ragged row {b} LSE")
+        # a row whose prefix is empty sees only draft tokens: the cache may be anything
+        x2 = dict(x, k_cache=x["k_cache"].copy(), v_cache=x["v_cache"].copy())
+        x2["k_cache"][1] = 1e3
+        x2["v_cache"][1] = -7.0
+        O2, _ = _call(attn, x2, plens, S, L, 0.45, pass_)
+        _close(O2[1], O[1], tol=0.0, what="cache of an empty-prefix row")
+
+
+def check_ragged_bruteforce(attn):
+    """Per-row prefix lengths against the scalar-loop brute force."""
+    x = _inputs(61, 2, 2, 1, 4, 4, 2, 2, C=4)
+    for pass_ in (PASS_DIFFUSION, PASS_AR_INFILL):
+        O, lse = _call(attn, x, [3, 1], 2, 2, 0.7, pass_)
+        Ob, lseb = oracle.slot_attention_loops(x["q"], x["k_cache"], x["v_cache"], x["k_slot"], x["v_slot"],
+                                               [3, 1], 2, 2, 0.7, pass_)
+        _close(O, Ob, tol=1e-12, what="ragged brute force O")
+        _close(lse, lseb, tol=1e-12, what="ragged brute force LSE")
+
+
 ATTENTION_CHECKS = [
+    check_ragged_rows,
+    check_ragged_bruteforce,
     check_decode_l1,
     check_prefill_s1,
     check_blockdiag_p0,
@@ -367,3 +402,107 @@ def check_select_golden(select):
 
 
 SELECTION_CHECKS = [check_select_golden]
+
+
+# ------------------------------------------------------- verification
+
+
+def load_accept_golden():
+    with open(os.path.join(GOLDEN, "accept_cases.json")) as f:
+        return json.load(f)["cases"]
+
+
+def check_accept_golden(accept):
+    """Hand cases of the acceptance rule (Sec. 5.2 verification, threshold from Sec. 6)."""
+    for case in load_accept_golden():
+        tp = np.array(case["token_prob"], dtype=np.float32)[None]
+        sel = np.array(case["selected"], dtype=np.int32)[None]
+        acc, n, tot = accept(tp, sel, np.float32(case["threshold"]), case["rule"])
+        exp = np.array(case["expect"], dtype=np.uint8)
+        assert np.array_equal(acc[0], exp), f"{case['name']}: got {acc[0].tolist()}, expected {exp.tolist()}"
+        assert np.array_equal(n[0], exp.sum(axis=1)), f"{case['name']}: per-slot counts"
+        assert int(tot[0]) == int(exp.sum()), f"{case['name']}: total"
+
+
+def check_accept_invariants(accept):
+    """Random batches: accepted tokens pass the threshold, lie in selected
+    slots, form a leading run under the prefix rule, and the prefix rule
+    accepts a subset of what the per-token rule accepts."""
+    rng = np.random.default_rng(70)
+    B, S, L = 40, 6, 5
+    tp = rng.random((B, S, L)).astype(np.float32)
+    tp[rng.random((B, S, L)) < 0.1] = np.float32(0.4)
+    sel = np.full((B, S), -1, dtype=np.int32)
+    for b in range(B):
+        k = int(rng.integers(0, S + 1))
+        sel[b, :k] = rng.permutation(S)[:k]
+    thr = np.float32(0.4)
+    a_pre, n_pre, t_pre = accept(tp, sel, thr, oracle.ACCEPT_PREFIX)
+    a_tok, n_tok, t_tok = accept(tp, sel, thr, oracle.ACCEPT_PER_TOKEN)
+    for b in range(B):
+        chosen = set(int(s) for s in sel[b] if s >= 0)
+        for s in range(S):
+            if s not in chosen:
+                assert not a_pre[b, s].any() and not a_tok[b, s].any(), "unselected slot accepted"
+                continue
+            above = tp[b, s] > thr
+            assert np.array_equal(a_tok[b, s].astype(bool), above), "per-token rule"
+            run = 0
+            while run < L and above[run]:
+                run += 1
+            assert a_pre[b, s].tolist() == [1] * run + [0] * (L - run), "prefix rule is the leading run"
+    assert np.all(a_pre <= a_tok)
+    assert np.array_equal(n_pre, a_pre.sum(axis=2)) and np.array_equal(t_pre, n_pre.sum(axis=1))
+    assert np.array_equal(t_tok, a_tok.sum(axis=(1, 2)))
+
+
+def check_append_hand(append):
+    """A worked append: prefix of 2, slots taken in the order [1, 0]."""
+    B, Hkv, C, D, S, L = 1, 2, 7, 2, 2, 2
+    kc = np.full((B, Hkv, C, D), -1.0)
+    vc = np.full((B, Hkv, C, D), -2.0)
+    ks = np.arange(B * Hkv * S * L * D, dtype=np.float64).reshape(B, Hkv, S * L, D)
+    vs = 100.0 + ks
+    acc = np.array([[[1, 0], [1, 1]]], dtype=np.uint8)
+    kc2, vc2, lens = append(kc, vc, [2], ks, vs, acc, np.array([[1, 0]]))
+    assert lens.tolist() == [5]
+    # positions 2, 3, 4 take tokens 2, 3 (slot 1) then 0 (slot 0, position 0)
+    for g in range(Hkv):
+        assert np.array_equal(kc2[0, g, 2:5], ks[0, g, [2, 3, 0]])
+        assert np.array_equal(vc2[0, g, 2:5], vs[0, g, [2, 3, 0]])
+        assert np.all(kc2[0, g, :2] == -1.0) and np.all(kc2[0, g, 5:] == -1.0)
+        assert np.all(vc2[0, g, :2] == -2.0) and np.all(vc2[0, g, 5:] == -2.0)
+    # the same append into a cache of capacity 4 does not fit: the row is left as it was
+    kc3, vc3, lens3 = append(kc[:, :, :4], vc[:, :, :4], [2], ks, vs, acc, np.array([[1, 0]]))
+    assert lens3.tolist() == [2] and np.all(kc3 == -1.0) and np.all(vc3 == -2.0)
+
+
+def check_append_invariants(append):
+    """Random appends: the prefix and the tail of every row are untouched and
+    the appended rows are the accepted draft tokens, slot order then position
+    order."""
+    rng = np.random.default_rng(71)
+    B, Hkv, D, S, L, C = 5, 3, 4, 4, 3, 30
+    T = S * L
+    kc = rng.standard_normal((B, Hkv, C, D))
+    vc = rng.standard_normal((B, Hkv, C, D))
+    ks = rng.standard_normal((B, Hkv, T, D))
+    vs = rng.standard_normal((B, Hkv, T, D))
+    acc = (rng.random((B, S, L)) < 0.5).astype(np.uint8)
+    order = np.full((B, S), -1, dtype=np.int32)
+    for b in range(B):
+        k = int(rng.integers(0, S + 1))
+        order[b, :k] = rng.permutation(S)[:k]
+    plens = rng.integers(0, C - T + 1, B)
+    kc2, vc2, lens = append(kc, vc, plens, ks, vs, acc, order)
+    for b in range(B):
+        toks = [s * L + r for s in order[b] if s >= 0 for r in range(L) if acc[b, s, r]]
+        p0, n = int(plens[b]), len(toks)
+        assert int(lens[b]) == p0 + n
+        assert np.array_equal(kc2[b, :, :p0], kc[b, :, :p0]) and np.array_equal(kc2[b, :, p0 + n:], kc[b, :, p0 + n:])
+        assert np.array_equal(vc2[b, :, :p0], vc[b, :, :p0]) and np.array_equal(vc2[b, :, p0 + n:], vc[b, :, p0 + n:])
+        assert np.array_equal(kc2[b, :, p0:p0 + n], ks[b][:, toks]) and np.array_equal(vc2[b, :, p0:p0 + n], vs[b][:, toks])
+
+
+ACCEPT_CHECKS = [check_accept_golden, check_accept_invariants]
+APPEND_CHECKS = [check_append_hand, check_append_invariants]

@@ -188,6 +188,20 @@ def _sel_no_fallback(tc, op=None, cr=0, rule=0, threshold=0.9, k=1):
     return c, sel, n
 
 
+def _attn_ragged_uses_max(q, kc, vc, ks, vs, P, S, L, scale, pass_, **kw):
+    # every row uses the longest prefix of the batch
+    return oracle.slot_attention(q, kc, vc, ks, vs, int(np.max(P)), S, L, scale, pass_, **kw)
+
+
+def _attn_ragged_first_row(q, kc, vc, ks, vs, P, S, L, scale, pass_, **kw):
+    # every row uses the first row's prefix length
+    return oracle.slot_attention(q, kc, vc, ks, vs, int(np.ravel(P)[0]), S, L, scale, pass_, **kw)
+
+
+ATTENTION_MUTANTS["ragged prefix: longest for every row"] = _attn_ragged_uses_max
+ATTENTION_MUTANTS["ragged prefix: first row's for every row"] = _attn_ragged_first_row
+
+
 SELECTION_MUTANTS = {
     "threshold compared with >=": _sel_non_strict,
     "fallback takes the highest index on ties": _sel_fallback_highest_index,
@@ -221,3 +235,82 @@ def test_confidence_mutant_is_caught(name):
 @pytest.mark.parametrize("name", list(SELECTION_MUTANTS))
 def test_selection_mutant_is_caught(name):
     assert _caught(SELECTION_MUTANTS[name], pins.SELECTION_CHECKS), f"mutant '{name}' passed every pin"
+
+
+def _acc_non_strict(tp, sel, thr, rule=0):
+    return oracle.accept_tokens(tp, sel, np.nextafter(np.float32(thr), np.float32(-1)), rule)
+
+
+def _acc_prefix_is_per_token(tp, sel, thr, rule=0):
+    return oracle.accept_tokens(tp, sel, thr, oracle.ACCEPT_PER_TOKEN)
+
+
+def _acc_ignores_selection(tp, sel, thr, rule=0):
+    S = np.shape(tp)[1]
+    return oracle.accept_tokens(tp, np.tile(np.arange(S), (np.shape(tp)[0], 1)), thr, rule)
+
+
+def _acc_padding_skipped(tp, sel, thr, rule=0):
+    # a -1 entry is skipped instead of ending the list
+    sel = np.asarray(sel).copy()
+    for b in range(sel.shape[0]):
+        keep = [s for s in sel[b] if s >= 0]
+        sel[b] = keep + [-1] * (sel.shape[1] - len(keep))
+    return oracle.accept_tokens(tp, sel, thr, rule)
+
+
+def _acc_run_off_by_one(tp, sel, thr, rule=0):
+    acc, n, t = oracle.accept_tokens(tp, sel, thr, rule)
+    if rule == oracle.ACCEPT_PREFIX:
+        for b, s in zip(*np.nonzero(n)):
+            acc[b, s, n[b, s] - 1] = 0  # drops the last token of the run
+        n = acc.sum(axis=2).astype(np.int32)
+        t = n.sum(axis=1).astype(np.int32)
+    return acc, n, t
+
+
+ACCEPT_MUTANTS = {
+    "threshold compared with >=": _acc_non_strict,
+    "prefix rule accepts per token": _acc_prefix_is_per_token,
+    "unselected slots verified": _acc_ignores_selection,
+    "padding skipped instead of ending the list": _acc_padding_skipped,
+    "accepted run one short": _acc_run_off_by_one,
+}
+
+
+def _app_slot_order_ignored(kc, vc, pl, ks, vs, acc, order):
+    order = np.sort(np.where(np.asarray(order) < 0, 1 << 30, order), axis=1)
+    order = np.where(order == 1 << 30, -1, order)
+    return oracle.kv_append(kc, vc, pl, ks, vs, acc, order)
+
+
+def _app_off_by_one(kc, vc, pl, ks, vs, acc, order):
+    return oracle.kv_append(kc, vc, np.asarray(pl) + 1, ks, vs, acc, order)
+
+
+def _app_whole_slots(kc, vc, pl, ks, vs, acc, order):
+    acc = np.asarray(acc).copy()
+    acc[acc.any(axis=2)] = 1  # a partly accepted slot is appended whole
+    return oracle.kv_append(kc, vc, pl, ks, vs, acc, order)
+
+
+def _app_keys_for_values(kc, vc, pl, ks, vs, acc, order):
+    return oracle.kv_append(kc, vc, pl, ks, ks, acc, order)
+
+
+APPEND_MUTANTS = {
+    "slots appended in slot order": _app_slot_order_ignored,
+    "appended one position late": _app_off_by_one,
+    "partly accepted slots appended whole": _app_whole_slots,
+    "keys written as values": _app_keys_for_values,
+}
+
+
+@pytest.mark.parametrize("name", list(ACCEPT_MUTANTS))
+def test_accept_mutant_is_caught(name):
+    assert _caught(ACCEPT_MUTANTS[name], pins.ACCEPT_CHECKS), f"mutant '{name}' passed every pin"
+
+
+@pytest.mark.parametrize("name", list(APPEND_MUTANTS))
+def test_append_mutant_is_caught(name):
+    assert _caught(APPEND_MUTANTS[name], pins.APPEND_CHECKS), f"mutant '{name}' passed every pin"

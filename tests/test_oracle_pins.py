@@ -22,6 +22,16 @@ def test_selection_pin(check):
     check(oracle.select_slots)
 
 
+@pytest.mark.parametrize("check", pins.ACCEPT_CHECKS, ids=lambda f: f.__name__)
+def test_accept_pin(check):
+    check(oracle.accept_tokens)
+
+
+@pytest.mark.parametrize("check", pins.APPEND_CHECKS, ids=lambda f: f.__name__)
+def test_append_pin(check):
+    check(oracle.kv_append)
+
+
 def test_attention_probabilities_sum_to_one():
     x = pins._inputs(31, 2, 4, 2, 8, 5, 3, 4)
     for pass_ in (oracle.PASS_DIFFUSION, oracle.PASS_AR_INFILL):
