@@ -259,6 +259,8 @@ def main():
         log("timing the AR_INFILL (verification) pass")
         ms_ar, mean_ar, _ = timed(Z.PASS_AR_INFILL, max(10, args.steps // 2), 3)
         result["ar_infill_pass"] = {"steps_per_s": 1e3 / ms_ar, "slot_attn_us": mean_ar[0] * 1e3}
+        log("timing the verification step")
+        result["verification_step"] = verification_step(dev, wl, sets[0], conf_out, sel_out, max(10, args.steps // 2))
         del sets
         torch.cuda.empty_cache()
         result["layout_attention"] = layout_attention(dev, max(5, args.steps // 10))
@@ -267,6 +269,72 @@ def main():
         log("timing the float64 CPU oracle (reference baseline)")
         result["cpu_baseline"] = cpu_baseline(wl, x, c)
     print(json.dumps(result), flush=True)
+
+
+def verification_step(dev, wl, s, conf_out, sel_out, K):
+    """The step after scoring (Sec. 5.2 "Verification phase", "KV cache
+    update"): AR_INFILL attention of the draft tokens, confidence of the draft
+    ids (the scoring step's argmax) as targets, acceptance of the selected
+    slots, and the append of the accepted tokens to a cache with room for them.
+    The prefix lengths are reset between steps, outside the timed events."""
+    import torch
+
+    import paper_2609_19868_amd as Z
+
+    B, Hq, Hkv, D, P, S, L = wl.batch, wl.n_q_heads, wl.n_kv_heads, wl.head_dim, wl.prefix_len, wl.n_slots, wl.slot_len
+    T = wl.T
+    kc = torch.empty((B, Hkv, P + T, D), dtype=torch.bfloat16, device=dev)
+    vc = torch.empty_like(kc)
+    kc[:, :, :P].copy_(s["k_cache"][:, :, :P])
+    vc[:, :, :P].copy_(s["v_cache"][:, :, :P])
+    plens0 = torch.full((B,), P, dtype=torch.int32, device=dev)
+    plens = plens0.clone()
+    targets = conf_out["argmax"].clone()
+    out = torch.empty((B, Hq, T, D), dtype=torch.bfloat16, device=dev)
+    lse = torch.empty((B, Hq, T), dtype=torch.float32, device=dev)
+    tout = {k: torch.empty_like(conf_out[k]) for k in ("max_prob", "argmax", "lse")}
+    tout["target_prob"] = torch.empty_like(conf_out["max_prob"])
+    acc_out = (torch.empty((B, S, L), dtype=torch.uint8, device=dev), torch.empty((B, S), dtype=torch.int32, device=dev),
+               torch.empty((B,), dtype=torch.int32, device=dev))
+    # random LM-head weights make every probability tiny: threshold 0 accepts every
+    # token of the selected slots, which is the copy-heavy end of the append
+    thr = 0.0
+    selected = sel_out[1]
+
+    def one(evs=None):
+        if evs:
+            evs[0].record()
+        Z.slot_attn(s["q"], kc, vc, s["k_slot"], s["v_slot"], S, L, pass_=Z.PASS_AR_INFILL, prefix_len=P,
+                    out=out, lse=lse, prefix_lens=plens)
+        if evs:
+            evs[1].record()
+        Z.slot_confidence(s["hidden"], s["w_vocab"], target_ids=targets, out=tout)
+        if evs:
+            evs[2].record()
+        Z.verify_accept(tout["target_prob"].view(B, S, L), selected, thr, Z.ACCEPT_PREFIX, out=acc_out)
+        if evs:
+            evs[3].record()
+        Z.kv_append(kc, vc, plens, s["k_slot"], s["v_slot"], acc_out[0], selected)
+        if evs:
+            evs[4].record()
+
+    for _ in range(3):
+        plens.copy_(plens0)
+        one()
+    torch.cuda.synchronize()
+    per = []
+    appended = []
+    for _ in range(K):
+        plens.copy_(plens0)
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+        one(evs)
+        torch.cuda.synchronize()
+        per.append([evs[j].elapsed_time(evs[j + 1]) * 1e3 for j in range(4)])
+        appended.append(float((plens - plens0).float().mean()))
+    m = [statistics.mean(p[j] for p in per) for j in range(4)]
+    return {"slot_attn_ar_infill_us": m[0], "slot_confidence_targets_us": m[1], "verify_accept_us": m[2],
+            "kv_append_us": m[3], "step_us": sum(m), "steps_per_s": 1e6 / sum(m),
+            "tokens_appended_per_row": statistics.mean(appended), "token_threshold": thr}
 
 
 def copy_calibration(dev, K):

@@ -13,6 +13,16 @@
  *   3. zarya_select_slots     slot confidence and first-hitting slot selection
  *                             (Sec. 5.2 "Slot selection"; Sec. 6 threshold 0.9).
  *
+ * and the verification step that follows it (Sec. 5.2 "Verification phase",
+ * "KV cache update") adds
+ *
+ *   4. zarya_verify_accept    token acceptance of the verified slots against the
+ *                             token threshold (Sec. 6: 0.4);
+ *   5. zarya_kv_append        the accepted tokens' K/V appended to the cache,
+ *                             after which the rows of a batch may hold prefixes
+ *                             of different lengths (zarya_slot_attn's
+ *                             prefix_lens).
+ *
  * Conventions for every entry point:
  *  - Tensor arguments are DEVICE pointers to dense row-major (C-contiguous)
  *    arrays whose shapes are given in the comments; the caller owns every
@@ -42,7 +52,7 @@ extern "C" {
 #endif
 
 #define ZARYA_VERSION_MAJOR 0
-#define ZARYA_VERSION_MINOR 1
+#define ZARYA_VERSION_MINOR 2
 
 typedef enum zarya_status {
   ZARYA_OK = 0,
@@ -74,11 +84,12 @@ typedef enum zarya_cross_slot {
 /* ------------------------------------------------------------------------ */
 /*
  * Physical order of one sequence (Sec. 5.2 "Reordering": masked tokens follow
- * the unmasked ones): the P committed prefix tokens, whose K/V live in the
+ * the unmasked ones): the P_b committed prefix tokens, whose K/V live in the
  * cache, then the draft slots 0..S-1 of L tokens each (T = S*L tokens), whose
  * own K/V are passed separately.  Draft token t = s*L + r (slot s, position r)
  * of query head h (KV head g = h / (Hq/Hkv)) attends to
- *   - every prefix key j < P (the cache is read-only; Sec. 5.1 KV reuse),
+ *   - every prefix key j < P_b (the cache is read-only; Sec. 5.1 KV reuse),
+ *     where P_b = prefix_lens[b] if given, else desc->prefix_len,
  *   - the keys of its own slot: all L of them in the DIFFUSION pass, those at
  *     positions r' <= r in the AR_INFILL pass,
  *   - with cross_slot = CAUSAL, also every key of slots s' < s.
@@ -92,7 +103,7 @@ typedef struct zarya_slot_attn_desc {
   int32_t n_q_heads;     /* Hq >= 1                                             */
   int32_t n_kv_heads;    /* Hkv >= 1, Hq % Hkv == 0                             */
   int32_t head_dim;      /* D: 64 or 128                                        */
-  int32_t prefix_len;    /* P >= 0 valid cache rows                             */
+  int32_t prefix_len;    /* P >= 0 valid cache rows (the largest, with prefix_lens) */
   int32_t kv_capacity;   /* C >= P: row count (token stride) of the cache arrays */
   int32_t n_slots;       /* S >= 1                                              */
   int32_t slot_len;      /* L >= 1                                              */
@@ -117,6 +128,9 @@ zarya_status zarya_slot_attn_workspace_size(const zarya_slot_attn_desc* desc, si
  * k_slot    [B, Hkv, T, D] dtype   the draft tokens' own keys
  * v_slot    [B, Hkv, T, D] dtype   the draft tokens' own values
  * slot_pass [B, S] uint8 or NULL   per-slot zarya_pass overriding desc->pass
+ * prefix_lens [B] int32 or NULL    per-row prefix length P_b (after zarya_kv_append
+ *                                  rows differ); values are clamped on the GPU to
+ *                                  [0, desc->prefix_len]; NULL = desc->prefix_len
  * out       [B, Hq, T, D]  dtype   attention output (bf16: round to nearest even)
  * lse       [B, Hq, T] float32 or NULL
  * workspace device buffer of at least zarya_slot_attn_workspace_size bytes
@@ -128,8 +142,8 @@ zarya_status zarya_slot_attn_workspace_size(const zarya_slot_attn_desc* desc, si
  */
 zarya_status zarya_slot_attn(const zarya_slot_attn_desc* desc, const void* q, const void* k_cache,
                              const void* v_cache, const void* k_slot, const void* v_slot,
-                             const uint8_t* slot_pass, void* out, float* lse, void* workspace,
-                             size_t workspace_bytes, hipStream_t stream);
+                             const uint8_t* slot_pass, const int32_t* prefix_lens, void* out, float* lse,
+                             void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
 /* 2. LM-head confidence: logits = hidden . W^T reduced per row on the fly   */
@@ -197,6 +211,72 @@ zarya_status zarya_select_slots(int32_t batch, int32_t n_slots, int32_t slot_len
                                 const uint8_t* slot_open, int32_t conf_rule, int32_t rule, float threshold,
                                 int32_t k, float* slot_conf, int32_t* selected, int32_t* n_selected,
                                 hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* 4. Verification: token acceptance                                         */
+/* ------------------------------------------------------------------------ */
+typedef enum zarya_accept_rule {
+  ZARYA_ACCEPT_PREFIX = 0,   /* the longest run of passing tokens from the slot's first token:
+                                an autoregressive pass scores token r given tokens < r, so a
+                                rejected token voids the scores after it                       */
+  ZARYA_ACCEPT_PER_TOKEN = 1 /* every passing token on its own                                   */
+} zarya_accept_rule;
+
+/*
+ * Sec. 5.2 "Verification phase": the selected slots get an autoregressive
+ * verification pass (zarya_slot_attn with AR_INFILL, then
+ * zarya_slot_confidence with the draft ids as target_ids); a draft token of a
+ * verified slot passes when its probability exceeds the token threshold
+ * (strict; Sec. 6 uses 0.4).  Tokens of slots not listed in `selected` are
+ * rejected.
+ *
+ * token_prob [B, S, L] float32    probability of each draft token (target_prob)
+ * selected   [B, S] int32         verified slots; the first -1 ends the list
+ *                                 (zarya_select_slots output); ids outside [0, S)
+ *                                 are skipped
+ * accepted   [B, S, L] uint8 out  1 = accepted
+ * n_accepted [B, S] int32 out     accepted tokens per slot
+ * n_total    [B] int32 out or NULL  accepted tokens per batch row
+ * Comparisons are made between float32 values.  Requires 1 <= S <= 1024 and
+ * 1 <= L <= 4096.
+ */
+zarya_status zarya_verify_accept(int32_t batch, int32_t n_slots, int32_t slot_len, const float* token_prob,
+                                 const int32_t* selected, float token_threshold, int32_t rule,
+                                 uint8_t* accepted, int32_t* n_accepted, int32_t* n_total, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* 5. KV-cache update: append the accepted tokens                            */
+/* ------------------------------------------------------------------------ */
+typedef struct zarya_kv_append_desc {
+  int32_t batch;       /* B >= 1                                              */
+  int32_t n_kv_heads;  /* Hkv >= 1                                            */
+  int32_t head_dim;    /* D: 64 or 128                                        */
+  int32_t kv_capacity; /* C: row count (token stride) of the cache arrays     */
+  int32_t n_slots;     /* S >= 1                                              */
+  int32_t slot_len;    /* L >= 1, S*L <= 8192                                 */
+  int32_t dtype;       /* zarya_dtype of the caches and the slot K/V          */
+} zarya_kv_append_desc;
+
+/*
+ * Sec. 5.2 "KV cache update": accepted tokens join the committed prefix, so
+ * they are never recomputed.  For each batch row b the K and V rows of its
+ * accepted draft tokens are copied to cache positions prefix_lens[b],
+ * prefix_lens[b] + 1, ... -- slots in the order given by `order` (the first -1
+ * ends it), positions in slot order -- and prefix_lens[b] grows by their
+ * number.  Attention over the cache does not depend on the order of its keys.
+ *
+ * k_slot, v_slot   [B, Hkv, S*L, D] dtype  the draft tokens' own K/V
+ * accepted         [B, S, L] uint8         nonzero = append
+ * order            [B, S] int32            slots in append order (e.g. `selected`);
+ *                                          ids outside [0, S) are skipped
+ * prefix_lens      [B] int32 in/out
+ * k_cache, v_cache [B, Hkv, C, D] dtype in/out
+ * A row whose prefix_lens[b] is negative or whose append would pass C is left
+ * unchanged, its length included (checked on the GPU).
+ */
+zarya_status zarya_kv_append(const zarya_kv_append_desc* desc, const void* k_slot, const void* v_slot,
+                             const uint8_t* accepted, const int32_t* order, int32_t* prefix_lens,
+                             void* k_cache, void* v_cache, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
 /* Diagnostics                                                               */

@@ -45,7 +45,8 @@ def accept_tokens(token_prob, selected, threshold, rule=ACCEPT_PREFIX):
 
     token_prob [B, S, L] float32: probability of each draft token under the
                verification pass
-    selected   [B, S] int: the verified slots, -1 padded at the end
+    selected   [B, S] int: the verified slots; the first -1 ends the list and
+               ids past S are skipped
     threshold  float32 token threshold (a token is accepted if p > threshold)
 
     Returns accepted [B, S, L] uint8 (1 = accepted), n_accepted [B, S] int32
@@ -61,6 +62,8 @@ def accept_tokens(token_prob, selected, threshold, rule=ACCEPT_PREFIX):
             s = int(sel[b, i])
             if s < 0:
                 break  # the rest of the row is padding
+            if s >= S:
+                continue  # not a slot id
             above = tp[b, s] > thr
             if rule == ACCEPT_PREFIX:
                 r = 0
@@ -80,7 +83,8 @@ def kv_append(k_cache, v_cache, prefix_lens, k_slot, v_slot, accepted, order):
     prefix_lens      [B]              valid prefix length of each batch row
     k_slot, v_slot   [B, Hkv, T, D]   the draft tokens' own K/V, T = S*L
     accepted         [B, S, L]        1 = accepted
-    order            [B, S]           slots in append order, -1 padded
+    order            [B, S]           slots in append order; the first -1 ends it,
+                                      ids past S are skipped
 
     A batch row whose appended length would exceed the capacity C is left
     unchanged.  Returns (k_cache', v_cache', prefix_lens').
@@ -99,6 +103,8 @@ def kv_append(k_cache, v_cache, prefix_lens, k_slot, v_slot, accepted, order):
             s = int(ordr[b, i])
             if s < 0:
                 break
+            if s >= S:
+                continue
             tokens += [s * L + r for r in range(L) if acc[b, s, r]]
         p0 = int(plens[b])
         if p0 < 0 or p0 + len(tokens) > C:

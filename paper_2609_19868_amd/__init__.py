@@ -7,6 +7,12 @@ The three calls of one scoring step of slotted speculative decoding
 * :func:`slot_confidence`  -- LM-head softmax statistics, logits kept on chip
 * :func:`select_slots`     -- first-hitting slot selection
 
+and the verification step after it (Sec. 5.2 "Verification phase", "KV cache
+update"):
+
+* :func:`verify_accept`    -- accepted tokens of the verified slots
+* :func:`kv_append`        -- the accepted tokens' K/V appended to the cache
+
 Each function marshals torch tensors (device memory) and torch's current
 stream into the C ABI of ``include/zarya.h``; all arithmetic runs in the HIP
 kernels.  Outputs and workspaces are allocated with torch unless passed in.
@@ -21,6 +27,8 @@ import torch
 
 from . import _lib
 from ._lib import (  # noqa: F401
+    ACCEPT_PER_TOKEN,
+    ACCEPT_PREFIX,
     CROSS_SLOT_CAUSAL,
     CROSS_SLOT_NONE,
     DTYPE_BF16,
@@ -39,7 +47,11 @@ __all__ = [
     "slot_attn_desc",
     "slot_confidence",
     "select_slots",
+    "verify_accept",
+    "kv_append",
     "ZaryaError",
+    "ACCEPT_PREFIX",
+    "ACCEPT_PER_TOKEN",
     "PASS_DIFFUSION",
     "PASS_AR_INFILL",
     "CROSS_SLOT_NONE",
@@ -87,11 +99,13 @@ def slot_attn_desc(q, k_cache, k_slot, n_slots, slot_len, pass_=PASS_DIFFUSION, 
 
 def slot_attn(q, k_cache, v_cache, k_slot, v_slot, n_slots, slot_len, pass_=PASS_DIFFUSION,
               cross_slot=CROSS_SLOT_NONE, slot_pass=None, prefix_len=None, softmax_scale=None,
-              out=None, lse=None, want_lse=True, workspace=None, prefix_splits=0):
+              out=None, lse=None, want_lse=True, workspace=None, prefix_splits=0, prefix_lens=None):
     """Attention of S draft slots x L tokens against a prefix KV cache.
 
     q [B,Hq,T,D], k_cache/v_cache [B,Hkv,C,D] (or None when there is no
-    prefix), k_slot/v_slot [B,Hkv,T,D], slot_pass [B,S] uint8 or None.
+    prefix), k_slot/v_slot [B,Hkv,T,D], slot_pass [B,S] uint8 or None,
+    prefix_lens [B] int32 per-row prefix lengths (each at most prefix_len,
+    which defaults to C) or None.
     Returns (out [B,Hq,T,D], lse [B,Hq,T] float32 or None).
     """
     B, Hq, T, D = q.shape
@@ -107,6 +121,8 @@ def slot_attn(q, k_cache, v_cache, k_slot, v_slot, n_slots, slot_len, pass_=PASS
         _need(v_cache, "v_cache", (B, Hkv, desc.kv_capacity, D), dt, dev)
     if slot_pass is not None:
         _need(slot_pass, "slot_pass", (B, n_slots), torch.uint8, dev)
+    if prefix_lens is not None:
+        _need(prefix_lens, "prefix_lens", (B,), torch.int32, dev)
     if out is None:
         out = torch.empty((B, Hq, T, D), dtype=dt, device=dev)
     _need(out, "out", (B, Hq, T, D), dt, dev)
@@ -119,7 +135,8 @@ def slot_attn(q, k_cache, v_cache, k_slot, v_slot, n_slots, slot_len, pass_=PASS
         workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     _lib.check(_lib.lib().zarya_slot_attn(
         ctypes.byref(desc), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(k_slot), _ptr(v_slot), _ptr(slot_pass),
-        _ptr(out), _ptr(lse), _ptr(workspace), 0 if workspace is None else workspace.numel(), _stream()))
+        _ptr(prefix_lens), _ptr(out), _ptr(lse), _ptr(workspace), 0 if workspace is None else workspace.numel(),
+        _stream()))
     return out, lse
 
 
@@ -178,3 +195,53 @@ def select_slots(token_conf, slot_open=None, conf_rule=SLOT_CONF_FIRST_TOKEN, ru
         B, S, L, _ptr(token_conf), _ptr(slot_open), int(conf_rule), int(rule), float(threshold), int(k),
         _ptr(slot_conf), _ptr(selected), _ptr(n_selected), _stream()))
     return slot_conf, selected, n_selected
+
+
+def verify_accept(token_prob, selected, token_threshold=0.4, rule=ACCEPT_PREFIX, out=None):
+    """Accepted draft tokens of the verified slots.
+
+    token_prob [B,S,L] float32 (probability of each draft token under the
+    verification pass), selected [B,S] int32 (verified slots, the first -1
+    ends the list).  Returns (accepted [B,S,L] uint8, n_accepted [B,S] int32,
+    n_total [B] int32).
+    """
+    B, S, L = token_prob.shape
+    dev = token_prob.device
+    _need(token_prob, "token_prob", (B, S, L), torch.float32, dev)
+    _need(selected, "selected", (B, S), torch.int32, dev)
+    if out is None:
+        out = (
+            torch.empty((B, S, L), dtype=torch.uint8, device=dev),
+            torch.empty((B, S), dtype=torch.int32, device=dev),
+            torch.empty((B,), dtype=torch.int32, device=dev),
+        )
+    accepted, n_accepted, n_total = out
+    _lib.check(_lib.lib().zarya_verify_accept(
+        B, S, L, _ptr(token_prob), _ptr(selected), float(token_threshold), int(rule), _ptr(accepted),
+        _ptr(n_accepted), _ptr(n_total), _stream()))
+    return accepted, n_accepted, n_total
+
+
+def kv_append(k_cache, v_cache, prefix_lens, k_slot, v_slot, accepted, order):
+    """Append the accepted draft tokens' K/V after each row's prefix, in place.
+
+    k_cache/v_cache [B,Hkv,C,D] (updated), prefix_lens [B] int32 (updated),
+    k_slot/v_slot [B,Hkv,S*L,D], accepted [B,S,L] uint8, order [B,S] int32
+    (slots in append order, the first -1 ends it).
+    """
+    B, Hkv, C, D = k_cache.shape
+    _, S, L = accepted.shape
+    dev, dt = k_cache.device, k_cache.dtype
+    _need(k_cache, "k_cache", (B, Hkv, C, D), dt, dev)
+    _need(v_cache, "v_cache", (B, Hkv, C, D), dt, dev)
+    _need(k_slot, "k_slot", (B, Hkv, S * L, D), dt, dev)
+    _need(v_slot, "v_slot", (B, Hkv, S * L, D), dt, dev)
+    _need(accepted, "accepted", (B, S, L), torch.uint8, dev)
+    _need(order, "order", (B, S), torch.int32, dev)
+    _need(prefix_lens, "prefix_lens", (B,), torch.int32, dev)
+    desc = _lib.KvAppendDesc(batch=B, n_kv_heads=Hkv, head_dim=D, kv_capacity=C, n_slots=S, slot_len=L,
+                             dtype=_DT[dt])
+    _lib.check(_lib.lib().zarya_kv_append(
+        ctypes.byref(desc), _ptr(k_slot), _ptr(v_slot), _ptr(accepted), _ptr(order), _ptr(prefix_lens),
+        _ptr(k_cache), _ptr(v_cache), _stream()))
+    return k_cache, v_cache, prefix_lens

@@ -30,6 +30,8 @@ SLOT_CONF_FIRST_TOKEN = 0
 SLOT_CONF_MEAN = 1
 SELECT_THRESHOLD = 0
 SELECT_TOP_K = 1
+ACCEPT_PREFIX = 0
+ACCEPT_PER_TOKEN = 1
 
 # every symbol include/zarya.h declares
 EXPORTS = (
@@ -38,6 +40,8 @@ EXPORTS = (
     "zarya_slot_confidence_workspace_size",
     "zarya_slot_confidence",
     "zarya_select_slots",
+    "zarya_verify_accept",
+    "zarya_kv_append",
     "zarya_status_string",
     "zarya_last_error",
     "zarya_version",
@@ -71,6 +75,18 @@ class ConfDesc(ctypes.Structure):
     ]
 
 
+class KvAppendDesc(ctypes.Structure):
+    _fields_ = [
+        ("batch", ctypes.c_int32),
+        ("n_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("kv_capacity", ctypes.c_int32),
+        ("n_slots", ctypes.c_int32),
+        ("slot_len", ctypes.c_int32),
+        ("dtype", ctypes.c_int32),
+    ]
+
+
 class ZaryaError(RuntimeError):
     def __init__(self, status, message):
         super().__init__(f"{status_name(status)}: {message}")
@@ -93,7 +109,7 @@ def lib():
         vp, sz, i32, f32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32, ctypes.c_float
         L.zarya_slot_attn_workspace_size.argtypes = [ctypes.POINTER(SlotAttnDesc), ctypes.POINTER(sz)]
         L.zarya_slot_attn_workspace_size.restype = ctypes.c_int
-        L.zarya_slot_attn.argtypes = [ctypes.POINTER(SlotAttnDesc), vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.zarya_slot_attn.argtypes = [ctypes.POINTER(SlotAttnDesc), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         L.zarya_slot_attn.restype = ctypes.c_int
         L.zarya_slot_confidence_workspace_size.argtypes = [ctypes.POINTER(ConfDesc), ctypes.POINTER(sz)]
         L.zarya_slot_confidence_workspace_size.restype = ctypes.c_int
@@ -101,6 +117,10 @@ def lib():
         L.zarya_slot_confidence.restype = ctypes.c_int
         L.zarya_select_slots.argtypes = [i32, i32, i32, vp, vp, i32, i32, f32, i32, vp, vp, vp, vp]
         L.zarya_select_slots.restype = ctypes.c_int
+        L.zarya_verify_accept.argtypes = [i32, i32, i32, vp, vp, f32, i32, vp, vp, vp, vp]
+        L.zarya_verify_accept.restype = ctypes.c_int
+        L.zarya_kv_append.argtypes = [ctypes.POINTER(KvAppendDesc), vp, vp, vp, vp, vp, vp, vp, vp]
+        L.zarya_kv_append.restype = ctypes.c_int
         L.zarya_status_string.argtypes = [ctypes.c_int]
         L.zarya_status_string.restype = ctypes.c_char_p
         L.zarya_last_error.argtypes = []

@@ -5,6 +5,7 @@
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <algorithm>
 #include <string>
 
 #include "kernels.hpp"
@@ -179,8 +180,9 @@ zarya_status zarya_slot_attn_workspace_size(const zarya_slot_attn_desc* desc, si
 }
 
 zarya_status zarya_slot_attn(const zarya_slot_attn_desc* d, const void* q, const void* k_cache, const void* v_cache,
-                             const void* k_slot, const void* v_slot, const uint8_t* slot_pass, void* out, float* lse,
-                             void* workspace, size_t workspace_bytes, hipStream_t stream) {
+                             const void* k_slot, const void* v_slot, const uint8_t* slot_pass,
+                             const int32_t* prefix_lens, void* out, float* lse, void* workspace,
+                             size_t workspace_bytes, hipStream_t stream) {
   zarya_status st = check_attn_desc(d);
   if (st != ZARYA_OK) return st;
   if (!q || !k_slot || !v_slot || !out) return fail(ZARYA_ERR_INVALID_ARGUMENT, "q, k_slot, v_slot and out are required");
@@ -201,6 +203,7 @@ zarya_status zarya_slot_attn(const zarya_slot_attn_desc* d, const void* q, const
     p.k_slot = static_cast<const float*>(k_slot);
     p.v_slot = static_cast<const float*>(v_slot);
     p.slot_pass = slot_pass;
+    p.prefix_lens = prefix_lens;
     p.out = static_cast<float*>(out);
     p.lse = lse;
     p.B = d->batch;
@@ -226,6 +229,7 @@ zarya_status zarya_slot_attn(const zarya_slot_attn_desc* d, const void* q, const
   p.k_slot = static_cast<const uint16_t*>(k_slot);
   p.v_slot = static_cast<const uint16_t*>(v_slot);
   p.slot_pass = slot_pass;
+  p.prefix_lens = prefix_lens;
   p.out = static_cast<uint16_t*>(out);
   p.lse = lse;
   if (pl.n_split > 1) {
@@ -345,6 +349,70 @@ zarya_status zarya_select_slots(int32_t batch, int32_t n_slots, int32_t slot_len
   p.selected = selected;
   p.n_selected = n_selected;
   return hip_status(launch_select_slots(p, stream), "select_slots launch");
+}
+
+zarya_status zarya_verify_accept(int32_t batch, int32_t n_slots, int32_t slot_len, const float* token_prob,
+                                 const int32_t* selected, float token_threshold, int32_t rule, uint8_t* accepted,
+                                 int32_t* n_accepted, int32_t* n_total, hipStream_t stream) {
+  if (batch < 1 || batch > 65535) return fail(ZARYA_ERR_INVALID_ARGUMENT, "batch must be in [1, 65535]");
+  if (n_slots < 1 || slot_len < 1) return fail(ZARYA_ERR_INVALID_ARGUMENT, "n_slots and slot_len must be >= 1");
+  if (n_slots > 1024) return fail(ZARYA_ERR_UNSUPPORTED, "n_slots %d exceeds 1024", n_slots);
+  if (slot_len > 4096) return fail(ZARYA_ERR_UNSUPPORTED, "slot_len %d exceeds 4096", slot_len);
+  if (rule != ZARYA_ACCEPT_PREFIX && rule != ZARYA_ACCEPT_PER_TOKEN)
+    return fail(ZARYA_ERR_INVALID_ARGUMENT, "unknown acceptance rule %d", rule);
+  if (isnan(token_threshold)) return fail(ZARYA_ERR_INVALID_ARGUMENT, "token_threshold is NaN");
+  if (!token_prob || !selected || !accepted || !n_accepted)
+    return fail(ZARYA_ERR_INVALID_ARGUMENT, "token_prob, selected, accepted and n_accepted are required");
+  (void)hipGetLastError();
+  AcceptParams p{};
+  p.B = batch;
+  p.S = n_slots;
+  p.L = slot_len;
+  p.token_prob = token_prob;
+  p.selected = selected;
+  p.threshold = token_threshold;
+  p.rule = rule;
+  p.accepted = accepted;
+  p.n_accepted = n_accepted;
+  p.n_total = n_total;
+  return hip_status(launch_verify_accept(p, stream), "verify_accept launch");
+}
+
+zarya_status zarya_kv_append(const zarya_kv_append_desc* d, const void* k_slot, const void* v_slot,
+                             const uint8_t* accepted, const int32_t* order, int32_t* prefix_lens, void* k_cache,
+                             void* v_cache, hipStream_t stream) {
+  if (!d) return fail(ZARYA_ERR_INVALID_ARGUMENT, "desc is NULL");
+  if (d->batch < 1 || d->batch > 65535) return fail(ZARYA_ERR_INVALID_ARGUMENT, "batch must be in [1, 65535]");
+  if (d->n_kv_heads < 1 || d->n_slots < 1 || d->slot_len < 1 || d->kv_capacity < 0)
+    return fail(ZARYA_ERR_INVALID_ARGUMENT, "n_kv_heads, n_slots and slot_len must be >= 1, kv_capacity >= 0");
+  if (d->dtype != ZARYA_DTYPE_F32 && d->dtype != ZARYA_DTYPE_BF16)
+    return fail(ZARYA_ERR_INVALID_ARGUMENT, "unknown dtype %d", d->dtype);
+  if (d->head_dim != 64 && d->head_dim != 128)
+    return fail(ZARYA_ERR_UNSUPPORTED, "head_dim %d is not supported (64 or 128)", d->head_dim);
+  if (d->n_slots > 1024) return fail(ZARYA_ERR_UNSUPPORTED, "n_slots %d exceeds 1024", d->n_slots);
+  if ((int64_t)d->n_slots * d->slot_len > kAppendMaxTokens)
+    return fail(ZARYA_ERR_UNSUPPORTED, "n_slots * slot_len exceeds %d", kAppendMaxTokens);
+  if ((int64_t)d->batch * d->n_kv_heads * std::max<int64_t>(d->kv_capacity, (int64_t)d->n_slots * d->slot_len) >
+      kI32Max)
+    return fail(ZARYA_ERR_UNSUPPORTED, "problem too large: batch*heads*tokens must stay below 2^31");
+  if (!k_slot || !v_slot || !accepted || !order || !prefix_lens || !k_cache || !v_cache)
+    return fail(ZARYA_ERR_INVALID_ARGUMENT, "every tensor argument is required");
+  (void)hipGetLastError();
+  AppendParams p{};
+  p.B = d->batch;
+  p.Hkv = d->n_kv_heads;
+  p.C = d->kv_capacity;
+  p.S = d->n_slots;
+  p.L = d->slot_len;
+  p.row_bytes = d->head_dim * (d->dtype == ZARYA_DTYPE_BF16 ? 2 : 4);
+  p.k_slot = k_slot;
+  p.v_slot = v_slot;
+  p.accepted = accepted;
+  p.order = order;
+  p.prefix_lens = prefix_lens;
+  p.k_cache = k_cache;
+  p.v_cache = v_cache;
+  return hip_status(launch_kv_append(p, stream), "kv_append launch");
 }
 
 }  // extern "C"

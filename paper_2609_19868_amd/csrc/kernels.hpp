@@ -14,8 +14,9 @@ struct AttnParams {
   const uint16_t* v_cache;
   const uint16_t* k_slot;  // [B, Hkv, T, D]
   const uint16_t* v_slot;
-  const uint8_t* slot_pass;  // [B, S] or null
-  uint16_t* out;             // [B, Hq, T, D]
+  const uint8_t* slot_pass;    // [B, S] or null
+  const int32_t* prefix_lens;  // [B] or null (then P for every row)
+  uint16_t* out;               // [B, Hq, T, D]
   float* lse;                // [B, Hq, T] or null (natural log)
   float* part_o;             // [n_split, rows_total, D]  (n_split > 1)
   float* part_lse;           // [n_split, rows_total]     (n_split > 1, log2 units)
@@ -34,6 +35,7 @@ struct AttnParams32 {
   const float* k_slot;
   const float* v_slot;
   const uint8_t* slot_pass;
+  const int32_t* prefix_lens;
   float* out;
   float* lse;
   int B, Hq, Hkv, P, C, S, L, T, G;
@@ -83,6 +85,31 @@ struct SelectParams {
   int32_t* n_selected;
 };
 
+struct AcceptParams {
+  int B, S, L;
+  const float* token_prob;
+  const int32_t* selected;
+  float threshold;
+  int rule;
+  uint8_t* accepted;
+  int32_t* n_accepted;
+  int32_t* n_total;
+};
+
+struct AppendParams {
+  int B, Hkv, C, S, L, row_bytes;  // row_bytes = head_dim * element size, a multiple of 16
+  const void* k_slot;
+  const void* v_slot;
+  const uint8_t* accepted;
+  const int32_t* order;
+  int32_t* prefix_lens;
+  void* k_cache;
+  void* v_cache;
+};
+
+// largest S*L the append kernel stages in LDS
+constexpr int kAppendMaxTokens = 8192;
+
 constexpr int kAttnKeysPerTile = 64;
 constexpr int kAttnRowsPerBlock = 128;
 // hidden rows per workgroup tile and workgroup count the bf16 confidence
@@ -96,5 +123,7 @@ hipError_t launch_slot_conf_bf16(const ConfParams& p, hipStream_t stream);
 hipError_t launch_slot_conf_f32(const ConfParams& p, hipStream_t stream);
 hipError_t launch_slot_conf_merge(const ConfMergeParams& p, hipStream_t stream);
 hipError_t launch_select_slots(const SelectParams& p, hipStream_t stream);
+hipError_t launch_verify_accept(const AcceptParams& p, hipStream_t stream);
+hipError_t launch_kv_append(const AppendParams& p, hipStream_t stream);
 
 }  // namespace zarya

@@ -76,6 +76,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(ZARYA_ATTN_
   const int split = (w / p.n_rb) % p.n_split;
   const int bg = w / (p.n_rb * p.n_split);  // b * Hkv + g
   const int b = bg / p.Hkv;
+  // this batch row's prefix length (rows differ after KV-cache appends)
+  const int Pb = p.prefix_lens ? min(max(p.prefix_lens[b], 0), p.P) : p.P;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
@@ -98,7 +100,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(ZARYA_ATTN_
   // ---- key tiles of this workgroup: a range of prefix tiles, then (last
   // split only) the draft-token tiles covering every row's visible range.
   const int pre_begin = split * p.tiles_per_split;
-  const int pre_end = min(p.n_prefix_tiles, pre_begin + p.tiles_per_split);
+  const int pre_end = min((Pb + KT - 1) / KT, pre_begin + p.tiles_per_split);
   const int n_pre = max(0, pre_end - pre_begin);
   int slot_lo = 0, n_slot = 0;
   if (split == p.n_split - 1) {
@@ -154,7 +156,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(ZARYA_ATTN_
       key0 = (pre_begin + i) * KT;
       kp = kc;
       vp = vc;
-      valid = p.P - key0;
+      valid = Pb - key0;
     } else {
       key0 = slot_lo + (i - n_pre) * KT;
       kp = ks_;
@@ -266,9 +268,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(ZARYA_ATTN_
     // ---- online softmax; masks only on tiles that need them
     const bool is_slot = i >= n_pre;
     const int key0 = is_slot ? slot_lo + (i - n_pre) * KT : (pre_begin + i) * KT;
-    const bool full = !is_slot && key0 + KT <= p.P;
+    const bool full = !is_slot && key0 + KT <= Pb;
     const int lim_lo = is_slot ? vis_lo : key0;
-    const int lim_n = is_slot ? vis_hi - vis_lo : p.P - key0;
+    const int lim_n = is_slot ? vis_hi - vis_lo : Pb - key0;
     if (!full) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
@@ -447,7 +449,8 @@ __global__ __launch_bounds__(64) void slot_attn_f32_kernel(AttnParams32 p) {
     m = m_new;
   };
   const size_t cbase = ((size_t)b * p.Hkv + g) * p.C * D;
-  for (int j = 0; j < p.P; ++j) visit(p.k_cache + cbase + (size_t)j * D, p.v_cache + cbase + (size_t)j * D);
+  const int Pb = p.prefix_lens ? min(max(p.prefix_lens[b], 0), p.P) : p.P;
+  for (int j = 0; j < Pb; ++j) visit(p.k_cache + cbase + (size_t)j * D, p.v_cache + cbase + (size_t)j * D);
   const size_t sbase = ((size_t)b * p.Hkv + g) * p.T * D;
   for (int j = vis_lo; j < vis_hi; ++j) visit(p.k_slot + sbase + (size_t)j * D, p.v_slot + sbase + (size_t)j * D);
   float* orow = p.out + (size_t)gid * D;

@@ -35,7 +35,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_version_and_status_strings():
     L = _lib.lib()
-    assert L.zarya_version() == 1
+    assert L.zarya_version() == 2
     for code, name in [(0, "ZARYA_OK"), (1, "ZARYA_ERR_INVALID_ARGUMENT"), (2, "ZARYA_ERR_UNSUPPORTED"),
                        (3, "ZARYA_ERR_WORKSPACE_TOO_SMALL"), (4, "ZARYA_ERR_HIP")]:
         assert L.zarya_status_string(code).decode() == name
@@ -50,7 +50,7 @@ def _desc(**kw):
 
 def _attn_status(desc, ptr=1, ws=None, ws_bytes=0):
     p = ctypes.c_void_p(ptr) if ptr else None
-    return _lib.lib().zarya_slot_attn(ctypes.byref(desc), p, p, p, p, p, None, p, None, ws, ws_bytes, None)
+    return _lib.lib().zarya_slot_attn(ctypes.byref(desc), p, p, p, p, p, None, None, p, None, ws, ws_bytes, None)
 
 
 @pytest.mark.parametrize("bad,code", [
@@ -87,8 +87,8 @@ def test_slot_attn_rejects_null_pointers_and_small_workspace():
         assert _attn_status(d, ws=None, ws_bytes=need) == _lib.ERR_INVALID_ARGUMENT
     # a prefix needs the cache pointers
     p = ctypes.c_void_p(1)
-    assert _lib.lib().zarya_slot_attn(ctypes.byref(d), p, None, None, p, p, None, p, None, p, 1 << 40, None) == \
-        _lib.ERR_INVALID_ARGUMENT
+    assert _lib.lib().zarya_slot_attn(ctypes.byref(d), p, None, None, p, p, None, None, p, None, p, 1 << 40,
+                                      None) == _lib.ERR_INVALID_ARGUMENT
 
 
 def test_slot_attn_workspace_sizes():
@@ -146,6 +146,55 @@ def test_select_slots_rejects_bad_arguments(args, code):
     st = _lib.lib().zarya_select_slots(a["batch"], a["n_slots"], a["slot_len"], p, None, a["conf_rule"], a["rule"],
                                        a["threshold"], a["k"], p, p, p, None)
     assert st == code
+
+
+@pytest.mark.parametrize("args,code", [
+    (dict(batch=0), _lib.ERR_INVALID_ARGUMENT),
+    (dict(n_slots=0), _lib.ERR_INVALID_ARGUMENT),
+    (dict(slot_len=0), _lib.ERR_INVALID_ARGUMENT),
+    (dict(n_slots=2048), _lib.ERR_UNSUPPORTED),
+    (dict(slot_len=5000), _lib.ERR_UNSUPPORTED),
+    (dict(rule=2), _lib.ERR_INVALID_ARGUMENT),
+    (dict(threshold=float("nan")), _lib.ERR_INVALID_ARGUMENT),
+    (dict(ptr=0), _lib.ERR_INVALID_ARGUMENT),
+])
+def test_verify_accept_rejects_bad_arguments(args, code):
+    a = dict(batch=4, n_slots=8, slot_len=4, threshold=0.4, rule=0, ptr=1)
+    a.update(args)
+    p = ctypes.c_void_p(a["ptr"]) if a["ptr"] else None
+    st = _lib.lib().zarya_verify_accept(a["batch"], a["n_slots"], a["slot_len"], p, p, a["threshold"], a["rule"],
+                                        p, p, None, None)
+    assert st == code
+    assert len(_lib.lib().zarya_last_error()) > 0
+
+
+@pytest.mark.parametrize("bad,code", [
+    (dict(batch=0), _lib.ERR_INVALID_ARGUMENT),
+    (dict(n_kv_heads=0), _lib.ERR_INVALID_ARGUMENT),
+    (dict(n_slots=0), _lib.ERR_INVALID_ARGUMENT),
+    (dict(kv_capacity=-1), _lib.ERR_INVALID_ARGUMENT),
+    (dict(dtype=5), _lib.ERR_INVALID_ARGUMENT),
+    (dict(head_dim=80), _lib.ERR_UNSUPPORTED),
+    (dict(n_slots=1025, slot_len=1), _lib.ERR_UNSUPPORTED),
+    (dict(n_slots=512, slot_len=32), _lib.ERR_UNSUPPORTED),
+    (dict(batch=4096, n_kv_heads=64, kv_capacity=1 << 14), _lib.ERR_UNSUPPORTED),
+])
+def test_kv_append_rejects_bad_descriptors(bad, code):
+    base = dict(batch=2, n_kv_heads=8, head_dim=128, kv_capacity=4096, n_slots=8, slot_len=8, dtype=1)
+    base.update(bad)
+    d = _lib.KvAppendDesc(**base)
+    p = ctypes.c_void_p(1)
+    assert _lib.lib().zarya_kv_append(ctypes.byref(d), p, p, p, p, p, p, p, None) == code
+    assert len(_lib.lib().zarya_last_error()) > 0
+
+
+def test_kv_append_requires_every_tensor():
+    d = _lib.KvAppendDesc(batch=2, n_kv_heads=8, head_dim=128, kv_capacity=4096, n_slots=8, slot_len=8, dtype=1)
+    p = ctypes.c_void_p(1)
+    for i in range(7):
+        args = [p] * 7
+        args[i] = None
+        assert _lib.lib().zarya_kv_append(ctypes.byref(d), *args, None) == _lib.ERR_INVALID_ARGUMENT
 
 
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):

@@ -107,6 +107,48 @@ def test_bf16_split_counts_agree_and_runs_are_bitwise_identical():
         assert np.abs(outs[splits][1] - outs[1][1]).max() < 1e-5
 
 
+RAGGED = [
+    # name, dtype, overrides: per-row prefix lengths after KV-cache appends
+    ("bf16_p300", "bf16", dict(batch=4, n_q_heads=4, n_kv_heads=2, prefix_len=300, kv_capacity=320, n_slots=5,
+                               slot_len=7)),
+    ("bf16_d64", "bf16", dict(batch=3, n_q_heads=4, n_kv_heads=2, head_dim=64, prefix_len=257, n_slots=4,
+                              slot_len=6)),
+    ("f32", "f32", dict(batch=3, n_q_heads=2, n_kv_heads=1, head_dim=64, prefix_len=70, n_slots=3, slot_len=4)),
+]
+
+
+@pytest.mark.parametrize("name,dtype,over", RAGGED, ids=[c[0] for c in RAGGED])
+def test_ragged_prefix_lengths(name, dtype, over):
+    """Rows with different prefix lengths (0, full, and between), with 1 and 3
+    prefix splits: every row against the oracle with its own length."""
+    dev = require_gpu()
+    wl = W.WORKLOADS["qwen0.6b"].replace(**over, dtype=dtype, hidden=0, vocab=0, seed=80)
+    xd, xf = attn_inputs_dev(wl, dev)
+    P = wl.prefix_len
+    plens = np.array([P, 0, P // 2 + 3, 1][: wl.batch], dtype=np.int32)
+    pl_dev = torch.from_numpy(plens).to(dev)
+    for pass_, pname in PASSES:
+        O, L = oracle.slot_attention(xf["q"], xf["k_cache"], xf["v_cache"], xf["k_slot"], xf["v_slot"], plens,
+                                     wl.n_slots, wl.slot_len, wl.scale, pass_)
+        for splits in (1, 3):
+            say(f"slot_attn ragged {name} {pname} splits={splits} plens={plens.tolist()}")
+            out, lse = Z.slot_attn(xd["q"], xd["k_cache"], xd["v_cache"], xd["k_slot"], xd["v_slot"], wl.n_slots,
+                                   wl.slot_len, pass_=pass_, prefix_len=P, softmax_scale=wl.scale,
+                                   prefix_splits=splits, prefix_lens=pl_dev)
+            torch.cuda.synchronize()
+            check_attn(to_f64(out), to_f64(lse), O, L, dtype, f"ragged {name} {pname} splits={splits}")
+    # out-of-range lengths are clamped to [0, prefix_len]
+    say(f"slot_attn ragged {name} clamped lengths")
+    wild = torch.tensor(([P + 50, -7, P, 0] * 2)[: wl.batch], dtype=torch.int32, device=dev)
+    out, lse = Z.slot_attn(xd["q"], xd["k_cache"], xd["v_cache"], xd["k_slot"], xd["v_slot"], wl.n_slots,
+                           wl.slot_len, prefix_len=P, softmax_scale=wl.scale, prefix_lens=wild)
+    torch.cuda.synchronize()
+    cl = np.clip(wild.cpu().numpy(), 0, P)
+    O, L = oracle.slot_attention(xf["q"], xf["k_cache"], xf["v_cache"], xf["k_slot"], xf["v_slot"], cl,
+                                 wl.n_slots, wl.slot_len, wl.scale, oracle.PASS_DIFFUSION)
+    check_attn(to_f64(out), to_f64(lse), O, L, dtype, f"ragged {name} clamped")
+
+
 def test_bf16_outputs_stay_inside_their_buffers():
     dev = require_gpu()
     wl = W.WORKLOADS["qwen0.6b"].replace(batch=1, n_q_heads=4, n_kv_heads=2, prefix_len=100, n_slots=3, slot_len=5,
