@@ -16,6 +16,8 @@ Language Model with Flexible Training and Dual-Mode Inference"):
   (Sec. 5.2 "probability of its first token", Table 1 tied embedding).
 * ``selection``   -- slot confidence and first-hitting slot selection
   (Sec. 5.2 slot selection, Sec. 6 inference settings).
+* ``sampling``    -- Gumbel-max sampling with temperature from a Philox4x32-10
+  stream (Sec. 5.2 "Sampling from categorical distribution", Sec. 5.1 step 3).
 * ``verify``      -- token acceptance after the verification pass and the
   KV-cache append of the accepted tokens (Sec. 5.2 "Verification phase",
   "KV cache update").
@@ -44,6 +46,7 @@ from .selection import (
     select_slots,
 )
 
+from .sampling import gumbel, philox4x32, slot_sample, uniforms
 from .verify import ACCEPT_PREFIX, ACCEPT_PER_TOKEN, accept_tokens, kv_append
 
 __all__ = [
@@ -67,4 +70,8 @@ __all__ = [
     "ACCEPT_PER_TOKEN",
     "accept_tokens",
     "kv_append",
+    "philox4x32",
+    "uniforms",
+    "gumbel",
+    "slot_sample",
 ]

@@ -506,3 +506,86 @@ def check_append_invariants(append):
 
 ACCEPT_CHECKS = [check_accept_golden, check_accept_invariants]
 APPEND_CHECKS = [check_append_hand, check_append_invariants]
+
+
+# ------------------------------------------------------------------ sampling
+
+# Known-answer vectors of Philox4x32-10 published with the generator (Salmon,
+# Moraes, Dror, Shaw, SC 2011; the Random123 distribution): (counter, key) ->
+# output words.
+PHILOX_KAT = [
+    ((0x00000000, 0x00000000, 0x00000000, 0x00000000), (0x00000000, 0x00000000),
+     (0x6627E8D5, 0xE169C58D, 0xBC57AC4C, 0x9B00DBD8)),
+    ((0xFFFFFFFF, 0xFFFFFFFF, 0xFFFFFFFF, 0xFFFFFFFF), (0xFFFFFFFF, 0xFFFFFFFF),
+     (0x408F276D, 0x41C83B0E, 0xA20BC7C6, 0x6D5451FD)),
+    ((0x243F6A88, 0x85A308D3, 0x13198A2E, 0x03707344), (0xA4093822, 0x299F31D0),
+     (0xD16CFE09, 0x94FDCCEB, 0x5001E420, 0x24126EA1)),
+]
+
+
+def check_philox_kat(philox):
+    for ctr, key, want in PHILOX_KAT:
+        got = tuple(int(x) for x in philox(np.array(ctr), np.array(key)))
+        assert got == want, f"Philox4x32-10 {ctr} {key}: {[hex(x) for x in got]}"
+
+
+def check_uniform_moments(unif):
+    """u strictly inside (0, 1), mean 1/2 and variance 1/12 within 5 sigma,
+    and different rows / offsets / seeds give different streams."""
+    u = unif(np.arange(1000), 1000, seed=7, offset=3)
+    n = u.size
+    assert u.min() > 0.0 and u.max() < 1.0
+    assert abs(u.mean() - 0.5) < 5 * np.sqrt(1 / 12 / n)
+    assert abs(u.var() - 1 / 12) < 5 * np.sqrt(1 / 180 / n)  # var of (u - 1/2)^2 is 1/180
+    assert not np.array_equal(u[0], u[1]), "rows share a stream"
+    assert not np.array_equal(unif([0], 1000, 7, 4), u[:1]), "offsets share a stream"
+    assert not np.array_equal(unif([0], 1000, 8, 3), u[:1]), "seeds share a stream"
+    # neighbouring ids are uncorrelated
+    assert abs(np.corrcoef(u[:, :-1].ravel(), u[:, 1:].ravel())[0, 1]) < 5 / np.sqrt(n)
+
+
+def check_gumbel_moments(unif):
+    """-ln(-ln u) has the standard Gumbel mean (Euler's gamma) and variance pi^2/6."""
+    g = oracle.gumbel(unif(np.arange(500), 2000, seed=11, offset=0))
+    n = g.size
+    assert abs(g.mean() - np.euler_gamma) < 5 * np.sqrt(np.pi ** 2 / 6 / n)
+    assert abs(g.var() - np.pi ** 2 / 6) < 0.02 * np.pi ** 2 / 6
+
+
+def _logit_rows(z, M):
+    """hidden / W such that every one of M rows has logits z (W = identity)."""
+    z = np.asarray(z, dtype=np.float64)
+    return np.tile(z, (M, 1)), np.eye(z.size)
+
+
+def check_sampling_distribution(sample):
+    """Gumbel-max: over many rows the drafted ids follow softmax(z / T)."""
+    z = np.array([1.2, -0.3, 0.0, 2.1, 0.7])
+    for T in (0.6, 1.7):
+        h, w = _logit_rows(z, 20000)
+        ids = sample(h, w, T, seed=5, offset=9)["sample_id"]
+        freq = np.bincount(ids, minlength=z.size) / ids.size
+        p = scipy.special.softmax(z / T)
+        sd = np.sqrt(p * (1 - p) / ids.size)
+        assert np.all(np.abs(freq - p) < 5 * sd), f"T={T}: frequencies {freq} vs softmax {p}"
+
+
+def check_sampling_cold_and_prob(sample):
+    """A tiny temperature gives the argmax; the reported probability is the
+    model's own softmax probability of the drafted id."""
+    rng = np.random.default_rng(12)
+    h = rng.standard_normal((40, 16))
+    w = rng.standard_normal((300, 16))
+    z = h @ w.T
+    r = sample(h, w, 1e-5, seed=1, offset=2)
+    assert np.array_equal(r["sample_id"], np.argmax(z, axis=1))
+    r = sample(h, w, 1.0, seed=1, offset=2)
+    p = scipy.special.softmax(z, axis=1)[np.arange(40), r["sample_id"]]
+    _close(r["sample_prob"], p, tol=1e-12, what="sample_prob")
+    _close(r["lse"], scipy.special.logsumexp(z, axis=1), tol=1e-12, what="sampling lse")
+    assert not np.array_equal(r["sample_id"], np.argmax(z, axis=1)), "T = 1 should not be greedy on 40 rows"
+
+
+PHILOX_CHECKS = [check_philox_kat]
+UNIFORM_CHECKS = [check_uniform_moments, check_gumbel_moments]
+SAMPLING_CHECKS = [check_sampling_distribution, check_sampling_cold_and_prob]

@@ -314,3 +314,110 @@ def test_accept_mutant_is_caught(name):
 @pytest.mark.parametrize("name", list(APPEND_MUTANTS))
 def test_append_mutant_is_caught(name):
     assert _caught(APPEND_MUTANTS[name], pins.APPEND_CHECKS), f"mutant '{name}' passed every pin"
+
+
+import oracle.sampling as osm  # noqa: E402
+
+_ORIG_PHILOX = osm.philox4x32
+_ORIG_UNIF = osm.uniforms
+_ORIG_GUMBEL = osm.gumbel
+
+
+def _philox_rounds9(c, k, rounds=10):
+    return _ORIG_PHILOX(c, k, rounds=9)
+
+
+def _philox_swapped_multipliers(c, k, rounds=10):
+    saved = osm.PHILOX_M0, osm.PHILOX_M1
+    osm.PHILOX_M0, osm.PHILOX_M1 = saved[1], saved[0]
+    try:
+        return _ORIG_PHILOX(c, k, rounds)
+    finally:
+        osm.PHILOX_M0, osm.PHILOX_M1 = saved
+
+
+def _philox_no_key_schedule(c, k, rounds=10):
+    saved = osm.PHILOX_W0, osm.PHILOX_W1
+    osm.PHILOX_W0, osm.PHILOX_W1 = 0, 0
+    try:
+        return _ORIG_PHILOX(c, k, rounds)
+    finally:
+        osm.PHILOX_W0, osm.PHILOX_W1 = saved
+
+
+PHILOX_MUTANTS = {
+    "nine rounds": _philox_rounds9,
+    "multipliers swapped": _philox_swapped_multipliers,
+    "key never bumped": _philox_no_key_schedule,
+}
+
+
+def _unif_block_word0(rows, vocab, seed, offset):
+    u = _ORIG_UNIF(rows, ((vocab + 3) // 4) * 4, seed, offset)
+    return np.repeat(u[:, ::4], 4, axis=1)[:, :vocab]  # one word for the four ids of a block
+
+
+def _unif_row_ignored(rows, vocab, seed, offset):
+    return np.repeat(_ORIG_UNIF([0], vocab, seed, offset), len(np.ravel(rows)), axis=0)
+
+
+def _unif_low_bits(rows, vocab, seed, offset):
+    u = _ORIG_UNIF(rows, vocab, seed, offset)
+    return np.mod(u * 256.0, 1.0) * 0.5  # a biased, squeezed uniform
+
+
+UNIFORM_MUTANTS = {
+    "one word for a whole block": _unif_block_word0,
+    "row not in the counter": _unif_row_ignored,
+    "biased uniforms": _unif_low_bits,
+}
+
+
+def _with_sampling(unif=None, gum=None):
+    def sample(*a, **kw):
+        saved = osm.uniforms, osm.gumbel
+        if unif is not None:
+            osm.uniforms = unif
+        if gum is not None:
+            osm.gumbel = gum
+        try:
+            return osm.slot_sample(*a, **kw)
+        finally:
+            osm.uniforms, osm.gumbel = saved
+    return sample
+
+
+def _sample_temperature_multiplied(h, w, T, seed, offset, row_chunk=256):
+    return osm.slot_sample(h, w, 1.0 / T, seed, offset, row_chunk)
+
+
+def _sample_prob_of_argmax(h, w, T, seed, offset, row_chunk=256):
+    r = osm.slot_sample(h, w, T, seed, offset, row_chunk)
+    z = np.asarray(h, np.float64) @ np.asarray(w, np.float64).T
+    r["sample_prob"] = np.exp(z.max(axis=1) - r["lse"])
+    return r
+
+
+SAMPLING_MUTANTS = {
+    "noise sign flipped": _with_sampling(gum=lambda u: np.log(-np.log(u))),
+    "exponential instead of Gumbel noise": _with_sampling(gum=lambda u: -np.log(u)),
+    "one word for a whole block": _with_sampling(unif=_unif_block_word0),
+    "row not in the counter": _with_sampling(unif=_unif_row_ignored),
+    "temperature multiplies": _sample_temperature_multiplied,
+    "probability of the argmax reported": _sample_prob_of_argmax,
+}
+
+
+@pytest.mark.parametrize("name", list(PHILOX_MUTANTS))
+def test_philox_mutant_is_caught(name):
+    assert _caught(PHILOX_MUTANTS[name], pins.PHILOX_CHECKS), f"mutant '{name}' passed every pin"
+
+
+@pytest.mark.parametrize("name", list(UNIFORM_MUTANTS))
+def test_uniform_mutant_is_caught(name):
+    assert _caught(UNIFORM_MUTANTS[name], pins.UNIFORM_CHECKS), f"mutant '{name}' passed every pin"
+
+
+@pytest.mark.parametrize("name", list(SAMPLING_MUTANTS))
+def test_sampling_mutant_is_caught(name):
+    assert _caught(SAMPLING_MUTANTS[name], pins.SAMPLING_CHECKS), f"mutant '{name}' passed every pin"

@@ -81,3 +81,18 @@ def test_select_threshold_always_returns_one_when_open():
     _, sel, n = oracle.select_slots(tc, None, oracle.CONF_FIRST_TOKEN, oracle.SELECT_THRESHOLD, 0.9, 1)
     assert np.all(n == 1)
     np.testing.assert_array_equal(sel[:, 0], np.argmax(tc[:, :, 0], axis=1))
+
+
+@pytest.mark.parametrize("check", pins.PHILOX_CHECKS, ids=lambda f: f.__name__)
+def test_philox_pin(check):
+    check(oracle.philox4x32)
+
+
+@pytest.mark.parametrize("check", pins.UNIFORM_CHECKS, ids=lambda f: f.__name__)
+def test_uniform_pin(check):
+    check(oracle.uniforms)
+
+
+@pytest.mark.parametrize("check", pins.SAMPLING_CHECKS, ids=lambda f: f.__name__)
+def test_sampling_pin(check):
+    check(oracle.slot_sample)
