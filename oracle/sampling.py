@@ -18,7 +18,8 @@ numbers: as easy as 1, 2, 3", SC 2011), written here from its published
 definition and checked against the published known-answer vectors.  The
 uniform for vocabulary entry v of row i comes from the block with counter
 (v >> 2, i, offset_lo, offset_hi) and key (seed_lo, seed_hi), output word
-v & 3: u = ((x >> 8) + 1/2) * 2^-24, strictly inside (0, 1).  G = -ln(-ln u).
+v & 3: u = ((x >> 9) + 1/2) * 2^-23, strictly inside (0, 1) and exactly
+representable in float32.  G = -ln(-ln u).
 
 Readings where the paper is silent (each listed in the design notes): the
 counter layout above; the reported probability of the drafted token is its
@@ -67,7 +68,7 @@ def uniforms(rows, vocab, seed, offset):
     ctr[..., 3] = (offset >> 32) & 0xFFFFFFFF
     key = np.array([seed & 0xFFFFFFFF, (seed >> 32) & 0xFFFFFFFF], dtype=np.uint64)
     x = philox4x32(ctr, key).reshape(rows.size, nb * 4)[:, :vocab]
-    return ((x >> 8).astype(np.float64) + 0.5) * 2.0 ** -24
+    return ((x >> 9).astype(np.float64) + 0.5) * 2.0 ** -23
 
 
 def gumbel(u):
