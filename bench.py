@@ -261,6 +261,8 @@ def main():
         result["ar_infill_pass"] = {"steps_per_s": 1e3 / ms_ar, "slot_attn_us": mean_ar[0] * 1e3}
         log("timing the verification step")
         result["verification_step"] = verification_step(dev, wl, sets[0], conf_out, sel_out, max(10, args.steps // 2))
+        log("timing the sampled LM-head reduction (Gumbel-max, T = 1)")
+        result["sampled_draft"] = sampled_draft(dev, wl, sets, max(10, args.steps // 2), conf_ms)
         del sets
         torch.cuda.empty_cache()
         result["layout_attention"] = layout_attention(dev, max(5, args.steps // 10))
@@ -335,6 +337,37 @@ def verification_step(dev, wl, s, conf_out, sel_out, K):
     return {"slot_attn_ar_infill_us": m[0], "slot_confidence_targets_us": m[1], "verify_accept_us": m[2],
             "kv_append_us": m[3], "step_us": sum(m), "steps_per_s": 1e6 / sum(m),
             "tokens_appended_per_row": statistics.mean(appended), "token_threshold": thr}
+
+
+def sampled_draft(dev, wl, sets, K, greedy_ms):
+    """Drafting with temperature (Sec. 5.2 "Sampling from categorical
+    distribution"): the LM-head reduction with Gumbel-max sampling fused in,
+    timed alone on the scoring step's hidden states, one Philox offset per
+    step."""
+    import torch
+
+    import paper_2609_19868_amd as Z
+    from paper_2609_19868_amd import _lib
+
+    M, H, V = wl.M, wl.hidden, wl.vocab
+    out = {k: torch.empty(M, dtype=torch.float32, device=dev) for k in ("sample_prob", "max_prob", "lse")}
+    out["sample_id"] = torch.empty(M, dtype=torch.int32, device=dev)
+    ws = torch.empty(_lib.slot_sample_workspace_size(_lib.ConfDesc(n_rows=M, hidden=H, vocab=V, dtype=1)),
+                     dtype=torch.uint8, device=dev)
+    for i in range(3):
+        Z.slot_sample(sets[i % len(sets)]["hidden"], sets[i % len(sets)]["w_vocab"], 1.0, 2024, i, out=out,
+                      workspace=ws)
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+    for i in range(K):
+        s = sets[i % len(sets)]
+        evs[i][0].record()
+        Z.slot_sample(s["hidden"], s["w_vocab"], 1.0, 2024, 100 + i, out=out, workspace=ws)
+        evs[i][1].record()
+    torch.cuda.synchronize()
+    us = statistics.mean(a.elapsed_time(b) for a, b in evs) * 1e3
+    return {"slot_sample_us": us, "tflops": 2.0 * M * V * H / (us * 1e-6) / 1e12,
+            "uniforms_per_s": M * V / (us * 1e-6), "vs_greedy_reduction": us / (greedy_ms * 1e3)}
 
 
 def copy_calibration(dev, K):

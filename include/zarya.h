@@ -23,6 +23,12 @@
  *                             of different lengths (zarya_slot_attn's
  *                             prefix_lens).
  *
+ * With a positive temperature the draft tokens are sampled instead of taken
+ * greedily (Sec. 5.2 "Sampling from categorical distribution"; Sec. 5.1):
+ *
+ *   6. zarya_slot_sample      Gumbel-max sampling fused into the LM-head
+ *                             reduction of 2.
+ *
  * Conventions for every entry point:
  *  - Tensor arguments are DEVICE pointers to dense row-major (C-contiguous)
  *    arrays whose shapes are given in the comments; the caller owns every
@@ -52,7 +58,7 @@ extern "C" {
 #endif
 
 #define ZARYA_VERSION_MAJOR 0
-#define ZARYA_VERSION_MINOR 2
+#define ZARYA_VERSION_MINOR 3
 
 typedef enum zarya_status {
   ZARYA_OK = 0,
@@ -277,6 +283,47 @@ typedef struct zarya_kv_append_desc {
 zarya_status zarya_kv_append(const zarya_kv_append_desc* desc, const void* k_slot, const void* v_slot,
                              const uint8_t* accepted, const int32_t* order, int32_t* prefix_lens,
                              void* k_cache, void* v_cache, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* 6. Sampled draft tokens: Gumbel-max inside the LM-head reduction          */
+/* ------------------------------------------------------------------------ */
+/*
+ * Sec. 5.2 "Sampling from categorical distribution" (and Sec. 5.1 step 3):
+ * with temperature T > 0 each draft token is drawn from softmax(z / T) by
+ * Gumbel-max, z_v = hidden[i,:] . w_vocab[v,:]:
+ *   sample_id[i]   = argmax_v (z_v / T + G_iv), ties to the smallest v
+ *   sample_prob[i] = exp(z_{sample_id[i]} - lse[i])  (model probability at
+ *                    T = 1: the drafted token's confidence, Sec. 5.2)
+ *   max_prob[i], lse[i] as in zarya_slot_confidence
+ * G_iv = -ln(-ln u_iv) with u_iv = ((x >> 9) + 1/2) * 2^-23, where x is word
+ * v & 3 of the Philox4x32-10 block (Salmon et al., SC 2011) with counter
+ * (v >> 2, i, offset_lo, offset_hi) and key (seed_lo, seed_hi) -- 32-bit
+ * halves of `seed` and `offset`.  The stream is fully determined by (seed,
+ * offset, i, v): advance `offset` between draft steps for fresh noise.  The
+ * perturbed scores are compared in float32 (in base 2:
+ * z log2(e) / T - log2(-log2 u), the same order).  Logits are never written to
+ * memory.
+ */
+typedef struct zarya_sample_params {
+  float temperature; /* T: finite, > 0                                      */
+  uint64_t seed;     /* Philox key                                          */
+  uint64_t offset;   /* Philox counter words 2 and 3                        */
+} zarya_sample_params;
+
+zarya_status zarya_slot_sample_workspace_size(const zarya_conf_desc* desc, size_t* bytes);
+
+/*
+ * hidden, w_vocab  as in zarya_slot_confidence
+ * sample_id   [M] int32       required
+ * sample_prob [M] float32     required
+ * max_prob    [M] float32 or NULL
+ * lse         [M] float32 or NULL
+ * workspace   at least zarya_slot_sample_workspace_size bytes
+ * Requires 1/T <= 1e30 (T not denormal-small).
+ */
+zarya_status zarya_slot_sample(const zarya_conf_desc* desc, const zarya_sample_params* params, const void* hidden,
+                               const void* w_vocab, int32_t* sample_id, float* sample_prob, float* max_prob,
+                               float* lse, void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
 /* Diagnostics                                                               */

@@ -76,24 +76,28 @@ def gumbel(u):
     return -np.log(-np.log(u))
 
 
-def slot_sample(hidden, w_vocab, temperature, seed, offset, row_chunk=256):
+def slot_sample(hidden, w_vocab, temperature, seed, offset, row_chunk=256, row_ids=None):
     """Gumbel-max sample of every row of logits = hidden . w_vocab^T.
 
+    ``row_ids`` are the rows' indices in the random stream (default 0..M-1;
+    given when ``hidden`` holds a subset of a larger batch).
     Returns a dict: ``sample_id`` (int64), ``sample_prob`` = softmax(z)[id],
     ``lse``, ``score_gap`` (top-2 gap of the perturbed scores z/T + G, to tell
-    decided rows from near-ties) and ``sample_logit``.
+    decided rows from near-ties), ``sample_logit`` and ``best_score`` (the
+    largest perturbed score).
     """
     h = np.asarray(hidden, dtype=np.float64)
     w = np.asarray(w_vocab, dtype=np.float64)
     M, V = h.shape[0], w.shape[0]
+    ids = np.arange(M) if row_ids is None else np.asarray(row_ids).reshape(M)
     T = float(temperature)
     assert T > 0
-    out = {k: np.empty(M) for k in ("sample_prob", "lse", "score_gap", "sample_logit")}
+    out = {k: np.empty(M) for k in ("sample_prob", "lse", "score_gap", "sample_logit", "best_score")}
     out["sample_id"] = np.empty(M, dtype=np.int64)
     for r0 in range(0, M, row_chunk):
         r1 = min(M, r0 + row_chunk)
         z = h[r0:r1] @ w.T
-        u = uniforms(np.arange(r0, r1), V, seed, offset)
+        u = uniforms(ids[r0:r1], V, seed, offset)
         score = z / T + gumbel(u)
         idx = np.argmax(score, axis=1)  # first (lowest) id on ties
         m = z.max(axis=1)
@@ -105,6 +109,7 @@ def slot_sample(hidden, w_vocab, temperature, seed, offset, row_chunk=256):
         else:
             gap = np.full(r1 - r0, np.inf)
         out["sample_id"][r0:r1] = idx
+        out["best_score"][r0:r1] = score[np.arange(r1 - r0), idx]
         out["sample_logit"][r0:r1] = zx
         out["lse"][r0:r1] = lse
         out["sample_prob"][r0:r1] = np.exp(zx - lse)

@@ -46,6 +46,7 @@ __all__ = [
     "slot_attn",
     "slot_attn_desc",
     "slot_confidence",
+    "slot_sample",
     "select_slots",
     "verify_accept",
     "kv_append",
@@ -169,6 +170,35 @@ def slot_confidence(hidden, w_vocab, target_ids=None, out=None, workspace=None):
     _lib.check(_lib.lib().zarya_slot_confidence(
         ctypes.byref(desc), _ptr(hidden), _ptr(w_vocab), _ptr(target_ids), _ptr(out["max_prob"]),
         _ptr(out["argmax"]), _ptr(out.get("lse")), _ptr(out.get("target_prob")), _ptr(workspace),
+        workspace.numel(), _stream()))
+    return out
+
+
+def slot_sample(hidden, w_vocab, temperature, seed, offset=0, out=None, workspace=None):
+    """Gumbel-max sample of every row of hidden . w_vocab^T at temperature T.
+
+    hidden [M,H], w_vocab [V,H] (bf16 or float32); seed and offset are the
+    64-bit Philox key and counter words (advance offset between draft steps).
+    Returns a dict with ``sample_id`` int32 [M], ``sample_prob`` (the sampled
+    token's probability at T = 1), ``max_prob`` and ``lse`` (float32 [M]).
+    """
+    M, H = hidden.shape
+    V = w_vocab.shape[0]
+    dev, dt = hidden.device, hidden.dtype
+    _need(hidden, "hidden", (M, H), dt, dev)
+    _need(w_vocab, "w_vocab", (V, H), dt, dev)
+    desc = _lib.ConfDesc(n_rows=M, hidden=H, vocab=V, dtype=_DT[dt])
+    params = _lib.SampleParams(temperature=float(temperature), seed=int(seed) & (2**64 - 1),
+                               offset=int(offset) & (2**64 - 1))
+    if out is None:
+        out = {k: torch.empty(M, dtype=torch.float32, device=dev) for k in ("sample_prob", "max_prob", "lse")}
+        out["sample_id"] = torch.empty(M, dtype=torch.int32, device=dev)
+    ws_bytes = _lib.slot_sample_workspace_size(desc)
+    if workspace is None:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    _lib.check(_lib.lib().zarya_slot_sample(
+        ctypes.byref(desc), ctypes.byref(params), _ptr(hidden), _ptr(w_vocab), _ptr(out["sample_id"]),
+        _ptr(out["sample_prob"]), _ptr(out.get("max_prob")), _ptr(out.get("lse")), _ptr(workspace),
         workspace.numel(), _stream()))
     return out
 

@@ -42,6 +42,8 @@ EXPORTS = (
     "zarya_select_slots",
     "zarya_verify_accept",
     "zarya_kv_append",
+    "zarya_slot_sample_workspace_size",
+    "zarya_slot_sample",
     "zarya_status_string",
     "zarya_last_error",
     "zarya_version",
@@ -72,6 +74,14 @@ class ConfDesc(ctypes.Structure):
         ("hidden", ctypes.c_int32),
         ("vocab", ctypes.c_int32),
         ("dtype", ctypes.c_int32),
+    ]
+
+
+class SampleParams(ctypes.Structure):
+    _fields_ = [
+        ("temperature", ctypes.c_float),
+        ("seed", ctypes.c_uint64),
+        ("offset", ctypes.c_uint64),
     ]
 
 
@@ -121,6 +131,11 @@ def lib():
         L.zarya_verify_accept.restype = ctypes.c_int
         L.zarya_kv_append.argtypes = [ctypes.POINTER(KvAppendDesc), vp, vp, vp, vp, vp, vp, vp, vp]
         L.zarya_kv_append.restype = ctypes.c_int
+        L.zarya_slot_sample_workspace_size.argtypes = [ctypes.POINTER(ConfDesc), ctypes.POINTER(sz)]
+        L.zarya_slot_sample_workspace_size.restype = ctypes.c_int
+        L.zarya_slot_sample.argtypes = [ctypes.POINTER(ConfDesc), ctypes.POINTER(SampleParams), vp, vp, vp, vp, vp,
+                                        vp, vp, sz, vp]
+        L.zarya_slot_sample.restype = ctypes.c_int
         L.zarya_status_string.argtypes = [ctypes.c_int]
         L.zarya_status_string.restype = ctypes.c_char_p
         L.zarya_last_error.argtypes = []
@@ -149,4 +164,10 @@ def slot_attn_workspace_size(desc: SlotAttnDesc) -> int:
 def slot_confidence_workspace_size(desc: ConfDesc) -> int:
     n = ctypes.c_size_t(0)
     check(lib().zarya_slot_confidence_workspace_size(ctypes.byref(desc), ctypes.byref(n)))
+    return n.value
+
+
+def slot_sample_workspace_size(desc: ConfDesc) -> int:
+    n = ctypes.c_size_t(0)
+    check(lib().zarya_slot_sample_workspace_size(ctypes.byref(desc), ctypes.byref(n)))
     return n.value

@@ -6,6 +6,7 @@
 #include <stdio.h>
 
 #include <algorithm>
+#include <cmath>
 #include <string>
 
 #include "kernels.hpp"
@@ -152,6 +153,70 @@ ConfPlan plan_conf(const zarya_conf_desc* d) {
   return pl;
 }
 
+// Sampling keeps two more partial arrays (best perturbed score and its id).
+size_t sample_ws_bytes(const zarya_conf_desc* d) {
+  const ConfPlan pl = plan_conf(d);
+  return pl.ws_bytes + 2 * align256((size_t)pl.n_vg * d->n_rows * 4);
+}
+
+// Enqueues the LM-head reduction and its merge; with `sp` also the sampling.
+// Arguments are already validated.
+zarya_status run_conf(const zarya_conf_desc* d, const zarya_sample_params* sp, const void* hidden,
+                      const void* w_vocab, const int32_t* target_ids, float* max_prob, int32_t* argmax_id, float* lse,
+                      float* target_prob, int32_t* sample_id, float* sample_prob, void* workspace,
+                      hipStream_t stream) {
+  const ConfPlan pl = plan_conf(d);
+  (void)hipGetLastError();
+  const size_t part = align256((size_t)pl.n_vg * d->n_rows * 4);
+  char* ws = static_cast<char*>(workspace);
+  ConfParams p{};
+  p.hidden = hidden;
+  p.w_vocab = w_vocab;
+  p.M = d->n_rows;
+  p.H = d->hidden;
+  p.V = d->vocab;
+  p.n_vg = pl.n_vg;
+  p.n_rt = pl.n_rt;
+  p.n_items = pl.n_vg * pl.n_rt;
+  p.per_xcd = (p.n_items + 7) / 8;
+  p.part_m = reinterpret_cast<float*>(ws);
+  p.part_s = reinterpret_cast<float*>(ws + part);
+  p.part_idx = reinterpret_cast<int*>(ws + 2 * part);
+  if (sp) {
+    p.part_g = reinterpret_cast<float*>(ws + 3 * part);
+    p.part_gi = reinterpret_cast<int*>(ws + 4 * part);
+    p.c2t = (float)(1.4426950408889634 / (double)sp->temperature);
+    p.seed_lo = (uint32_t)sp->seed;
+    p.seed_hi = (uint32_t)(sp->seed >> 32);
+    p.off_lo = (uint32_t)sp->offset;
+    p.off_hi = (uint32_t)(sp->offset >> 32);
+  }
+  hipError_t e = d->dtype == ZARYA_DTYPE_BF16 ? launch_slot_conf_bf16(p, stream) : launch_slot_conf_f32(p, stream);
+  if (e != hipSuccess) return hip_status(e, "LM-head reduction launch");
+
+  ConfMergeParams mp{};
+  mp.part_m = p.part_m;
+  mp.part_s = p.part_s;
+  mp.part_idx = p.part_idx;
+  mp.n_vg = pl.n_vg;
+  mp.M = d->n_rows;
+  mp.H = d->hidden;
+  mp.V = d->vocab;
+  mp.bf16 = d->dtype == ZARYA_DTYPE_BF16;
+  mp.hidden = hidden;
+  mp.w_vocab = w_vocab;
+  mp.target_ids = target_ids;
+  mp.max_prob = max_prob;
+  mp.argmax_id = argmax_id;
+  mp.lse = lse;
+  mp.target_prob = target_prob;
+  mp.part_g = p.part_g;
+  mp.part_gi = p.part_gi;
+  mp.sample_id = sample_id;
+  mp.sample_prob = sample_prob;
+  return hip_status(launch_slot_conf_merge(mp, stream), "LM-head merge launch");
+}
+
 }  // namespace
 
 extern "C" {
@@ -282,42 +347,36 @@ zarya_status zarya_slot_confidence(const zarya_conf_desc* d, const void* hidden,
     return fail(ZARYA_ERR_WORKSPACE_TOO_SMALL, "workspace of %zu bytes is below the %zu required", workspace_bytes,
                 pl.ws_bytes);
   if (!workspace) return fail(ZARYA_ERR_INVALID_ARGUMENT, "workspace is NULL");
-  (void)hipGetLastError();
+  return run_conf(d, nullptr, hidden, w_vocab, target_ids, max_prob, argmax_id, lse, target_prob, nullptr, nullptr,
+                  workspace, stream);
+}
 
-  const size_t part = align256((size_t)pl.n_vg * d->n_rows * 4);
-  ConfParams p{};
-  p.hidden = hidden;
-  p.w_vocab = w_vocab;
-  p.M = d->n_rows;
-  p.H = d->hidden;
-  p.V = d->vocab;
-  p.n_vg = pl.n_vg;
-  p.n_rt = pl.n_rt;
-  p.n_items = pl.n_vg * pl.n_rt;
-  p.per_xcd = (p.n_items + 7) / 8;
-  p.part_m = static_cast<float*>(workspace);
-  p.part_s = reinterpret_cast<float*>(static_cast<char*>(workspace) + part);
-  p.part_idx = reinterpret_cast<int*>(static_cast<char*>(workspace) + 2 * part);
-  hipError_t e = d->dtype == ZARYA_DTYPE_BF16 ? launch_slot_conf_bf16(p, stream) : launch_slot_conf_f32(p, stream);
-  if (e != hipSuccess) return hip_status(e, "slot_confidence launch");
+zarya_status zarya_slot_sample_workspace_size(const zarya_conf_desc* desc, size_t* bytes) {
+  if (!bytes) return fail(ZARYA_ERR_INVALID_ARGUMENT, "bytes is NULL");
+  zarya_status st = check_conf_desc(desc);
+  if (st != ZARYA_OK) return st;
+  *bytes = sample_ws_bytes(desc);
+  return ZARYA_OK;
+}
 
-  ConfMergeParams mp{};
-  mp.part_m = p.part_m;
-  mp.part_s = p.part_s;
-  mp.part_idx = p.part_idx;
-  mp.n_vg = pl.n_vg;
-  mp.M = d->n_rows;
-  mp.H = d->hidden;
-  mp.V = d->vocab;
-  mp.bf16 = d->dtype == ZARYA_DTYPE_BF16;
-  mp.hidden = hidden;
-  mp.w_vocab = w_vocab;
-  mp.target_ids = target_ids;
-  mp.max_prob = max_prob;
-  mp.argmax_id = argmax_id;
-  mp.lse = lse;
-  mp.target_prob = target_prob;
-  return hip_status(launch_slot_conf_merge(mp, stream), "slot_confidence merge launch");
+zarya_status zarya_slot_sample(const zarya_conf_desc* d, const zarya_sample_params* sp, const void* hidden,
+                               const void* w_vocab, int32_t* sample_id, float* sample_prob, float* max_prob,
+                               float* lse, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  zarya_status st = check_conf_desc(d);
+  if (st != ZARYA_OK) return st;
+  if (!sp) return fail(ZARYA_ERR_INVALID_ARGUMENT, "params is NULL");
+  const float T = sp->temperature;
+  if (!(T > 0.f) || !std::isfinite(T) || !(1.0 / (double)T <= 1e30))
+    return fail(ZARYA_ERR_INVALID_ARGUMENT, "temperature %g must be finite, > 0 and >= 1e-30", (double)T);
+  if (!hidden || !w_vocab || !sample_id || !sample_prob)
+    return fail(ZARYA_ERR_INVALID_ARGUMENT, "hidden, w_vocab, sample_id and sample_prob are required");
+  const size_t need = sample_ws_bytes(d);
+  if (workspace_bytes < need)
+    return fail(ZARYA_ERR_WORKSPACE_TOO_SMALL, "workspace of %zu bytes is below the %zu required", workspace_bytes,
+                need);
+  if (!workspace) return fail(ZARYA_ERR_INVALID_ARGUMENT, "workspace is NULL");
+  return run_conf(d, sp, hidden, w_vocab, nullptr, max_prob, nullptr, lse, nullptr, sample_id, sample_prob, workspace,
+                  stream);
 }
 
 zarya_status zarya_select_slots(int32_t batch, int32_t n_slots, int32_t slot_len, const float* token_conf,

@@ -107,6 +107,37 @@ __device__ __forceinline__ float max3f(float a, float b, float c) {
   return r;
 }
 
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC 2011): four 32-bit words from
+// a 128-bit counter and a 64-bit key.  Each round multiplies counter words 0
+// and 2 by the two round constants, swaps the halves of the products into the
+// other words under the round key, and bumps the key by the two Weyl constants.
+__device__ __forceinline__ uint4 philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3, uint32_t k0,
+                                               uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    const uint64_t p0 = (uint64_t)0xD2511F53u * c0;
+    const uint64_t p1 = (uint64_t)0xCD9E8D57u * c2;
+    const uint32_t n0 = (uint32_t)(p1 >> 32) ^ c1 ^ k0;
+    const uint32_t n2 = (uint32_t)(p0 >> 32) ^ c3 ^ k1;
+    c1 = (uint32_t)p1;
+    c3 = (uint32_t)p0;
+    c0 = n0;
+    c2 = n2;
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+  return make_uint4(c0, c1, c2, c3);
+}
+
+// Gumbel part of a perturbed score in the log2 domain: -log2(-log2 u) with
+// u = ((x >> 9) + 1/2) * 2^-23 in (0, 1), exact in float32.  Adding it to
+// z * log2(e) / T gives log2(e) * (z / T + G) up to a constant, G standard
+// Gumbel, so the argmax is the Gumbel-max sample.
+__device__ __forceinline__ float gumbel_log2(uint32_t x) {
+  const float u = fmaf((float)(x >> 9), 0x1p-23f, 0x1p-24f);  // exact: 2k+1 < 2^24
+  return -__builtin_amdgcn_logf(-__builtin_amdgcn_logf(u));
+}
+
 // Two floats -> packed bf16x2 (low half = a) with the hardware conversion
 // (round to nearest even).
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));

@@ -56,6 +56,13 @@ struct ConfParams {
   float* part_m;   // [M, n_vg]
   float* part_s;   // [M, n_vg]
   int* part_idx;   // [M, n_vg]
+  // Gumbel-max sampling (null part_g: no sampling).  Per (row, group): best
+  // perturbed score z*log2(e)/T - log2(-log2 u) and its id.  The bf16 path
+  // does not track the argmax when sampling (part_idx then holds INT_MAX).
+  float* part_g;
+  int* part_gi;
+  float c2t;  // log2(e) / temperature
+  uint32_t seed_lo, seed_hi, off_lo, off_hi;
 };
 
 struct ConfMergeParams {
@@ -71,6 +78,10 @@ struct ConfMergeParams {
   int32_t* argmax_id;
   float* lse;
   float* target_prob;
+  const float* part_g;  // sampling partials, or null
+  const int* part_gi;
+  int32_t* sample_id;
+  float* sample_prob;
 };
 
 struct SelectParams {

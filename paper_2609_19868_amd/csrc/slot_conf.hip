@@ -76,8 +76,8 @@ __device__ __forceinline__ int coff(int r, int ch) {
 // of vocab id id0 + c(ib, v), c = 32*ib + 8*(v/4) + v%4, for the lane's row of
 // row block jb; offsets c >= lim are past the vocabulary range.  The argmax
 // is searched only when the tile raises the running maximum; the lowest id at
-// the maximum wins (earlier tiles hold lower ids).
-template <int JB>
+// the maximum wins (earlier tiles hold lower ids).  ARGMAX = false skips it.
+template <int JB, bool ARGMAX = true>
 __device__ __forceinline__ void fold_tile(const f32x16 (&acc)[4][JB], int lim, int id0, float (&m_run)[JB],
                                           float (&s_run)[JB], int (&i_run)[JB]) {
   constexpr int IB = 4;
@@ -105,7 +105,7 @@ __device__ __forceinline__ void fold_tile(const f32x16 (&acc)[4][JB], int lim, i
           mt = fmaxf(mt, c < lim ? acc[ib][jb][v] : -INFINITY);
         }
     }
-    if (mt > m_run[jb]) {
+    if (ARGMAX && mt > m_run[jb]) {
       int it = 0;
       if (full) {
 #pragma unroll
@@ -150,25 +150,80 @@ __device__ __forceinline__ void fold_tile(const f32x16 (&acc)[4][JB], int lim, i
   }
 }
 
+// Sampling: fold one vocab tile into the running best perturbed score of the
+// lane's rows (same register layout as fold_tile; `row` = the lane's row of
+// row block 0, block jb holds row + 32*jb).  The uniforms of vocab ids
+// 4q..4q+3 of a row are the four words of the Philox block with counter
+// (q, row, off_lo, off_hi); a lane's ids come in aligned runs of four, so each
+// block is drawn once.  The strict comparison keeps the lowest id of equal
+// scores (ids grow along the scan).  Only the id is kept: the merge recomputes
+// the winner's logit.  The row blocks are the inner loop so that each range
+// test on the vocab offset serves all of them (hoisted across row blocks, the
+// tests' lane masks overflow the scalar registers).
+template <int JB>
+__device__ __forceinline__ void sample_fold(const f32x16 (&acc)[4][JB], int lim, int id0, int row,
+                                            const ConfParams& p, float (&g_best)[JB], int (&g_id)[JB]) {
+  const bool full = lim >= 128;
+#pragma unroll
+  for (int ib = 0; ib < 4; ++ib) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int c0 = ib * 32 + 8 * q;  // offsets c0 .. c0+3 hold ids id0 + c0 .. + 3
+#pragma unroll
+      for (int jb = 0; jb < JB; ++jb) {
+        const uint4 r = philox4x32_10((uint32_t)(id0 + c0) >> 2, (uint32_t)(row + 32 * jb), p.off_lo, p.off_hi,
+                                      p.seed_lo, p.seed_hi);
+        const uint32_t words[4] = {r.x, r.y, r.z, r.w};
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const float sc = fmaf(acc[ib][jb][4 * q + w], p.c2t, gumbel_log2(words[w]));
+          if ((full || c0 + w < lim) && sc > g_best[jb]) {
+            g_best[jb] = sc;
+            g_id[jb] = id0 + c0 + w;
+          }
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+}
+
+// Merge two sampling candidates: the higher score wins, the lower id on ties.
+__device__ __forceinline__ void sample_merge(float& g, int& gi, float g2, int gi2) {
+  if (g2 > g || (g2 == g && gi2 < gi)) {
+    g = g2;
+    gi = gi2;
+  }
+}
+
 // Combine the statistics of a workgroup's rows and write one partial per
 // (vocabulary group, row).  Lanes n and n+32 hold disjoint vocab ids of the
 // same row (merged by a shuffle); the waves of vocab halves 0 and 1 hold the
-// same rows (merged through `scratch`, 12 bytes per row).  Ends with a
+// same rows (merged through `scratch`, 20 bytes per row).  With SAMPLE the
+// sampling candidates are combined and written the same way (and the argmax,
+// not tracked then, is not written).  Contains a
 // workgroup barrier; `scratch` must be free of pending reads.
-template <int JB, int BR>
+template <int JB, int BR, bool SAMPLE>
 __device__ __forceinline__ void store_partials(const ConfParams& p, int vg, int row0, int rbase, int wv, int hh, int n,
                                                float (&m_run)[JB], float (&s_run)[JB], int (&i_run)[JB],
-                                               uint8_t* scratch) {
+                                               float (&g_best)[JB], int (&g_id)[JB], uint8_t* scratch) {
 #pragma unroll
   for (int jb = 0; jb < JB; ++jb) {
     const float m2 = __shfl_xor(m_run[jb], 32);
     const float s2 = __shfl_xor(s_run[jb], 32);
     const int i2 = __shfl_xor(i_run[jb], 32);
     stat_merge(m_run[jb], s_run[jb], i_run[jb], m2, s2, i2);
+    if constexpr (SAMPLE) {
+      const float g2 = __shfl_xor(g_best[jb], 32);
+      const int gi2 = __shfl_xor(g_id[jb], 32);
+      sample_merge(g_best[jb], g_id[jb], g2, gi2);
+    }
   }
   float* xm = reinterpret_cast<float*>(scratch);
   float* xs = xm + BR;
   int* xi = reinterpret_cast<int*>(xs + BR);
+  float* xg = reinterpret_cast<float*>(xi + BR);
+  int* xgi = reinterpret_cast<int*>(xg + BR);
   if (wv == 1 && hh == 0) {
 #pragma unroll
     for (int jb = 0; jb < JB; ++jb) {
@@ -176,6 +231,10 @@ __device__ __forceinline__ void store_partials(const ConfParams& p, int vg, int 
       xm[lr] = m_run[jb];
       xs[lr] = s_run[jb];
       xi[lr] = i_run[jb];
+      if constexpr (SAMPLE) {
+        xg[lr] = g_best[jb];
+        xgi[lr] = g_id[jb];
+      }
     }
   }
   __syncthreads();
@@ -185,11 +244,18 @@ __device__ __forceinline__ void store_partials(const ConfParams& p, int vg, int 
       const int lr = rbase + jb * 32 + n;
       stat_merge(m_run[jb], s_run[jb], i_run[jb], xm[lr], xs[lr], xi[lr]);
       const int row = row0 + lr;
+      const size_t o = (size_t)row * p.n_vg + vg;
       if (row < p.M) {
-        const size_t o = (size_t)row * p.n_vg + vg;
         p.part_m[o] = m_run[jb];
         p.part_s[o] = s_run[jb];
         p.part_idx[o] = i_run[jb];
+      }
+      if constexpr (SAMPLE) {
+        sample_merge(g_best[jb], g_id[jb], xg[lr], xgi[lr]);
+        if (row < p.M) {
+          p.part_g[o] = g_best[jb];
+          p.part_gi[o] = g_id[jb];
+        }
       }
     }
   }
@@ -201,7 +267,7 @@ __device__ __forceinline__ void store_partials(const ConfParams& p, int vg, int 
 // ring of NSW LDS buffers (prefetch distance NSW - 1 stages), the hidden tile
 // (re-read for every vocab tile, so served from L2) through a ring of NSX.
 // Partials are written per (vocabulary group, row).
-template <int NW, int BR, int BK, int NSW, int NSX>
+template <int NW, int BR, int BK, int NSW, int NSX, bool SAMPLE>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) void slot_conf_bf16_kernel(
     ConfParams p) {
   constexpr int ATB = BV * BK * 2;    // bytes of the W tile of one stage
@@ -322,11 +388,15 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
   f32x16 acc[IB][JB];  // set by the first k-step of every vocab tile
   float m_run[JB], s_run[JB];
   int i_run[JB];
+  float g_best[JB];  // sampling: best perturbed score and its id
+  int g_id[JB];
 #pragma unroll
   for (int j = 0; j < JB; ++j) {
     m_run[j] = kNegBig;
     s_run[j] = 0.f;
     i_run[j] = INT_MAX;
+    g_best[j] = -INFINITY;
+    g_id[j] = INT_MAX;
   }
 
   // Load order: iteration i issues the hidden tile of stage i+NSX-1, then the
@@ -407,11 +477,15 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
       }
     }
     if (i % nks == nks - 1) {
-      if (active) fold_tile<JB>(acc, v_hi - vbase - 4 * hh, vbase + 4 * hh, m_run, s_run, i_run);
+      if (active) {
+        fold_tile<JB, !SAMPLE>(acc, v_hi - vbase - 4 * hh, vbase + 4 * hh, m_run, s_run, i_run);
+        if constexpr (SAMPLE)
+          sample_fold<JB>(acc, v_hi - vbase - 4 * hh, vbase + 4 * hh, row0 + rbase + n, p, g_best, g_id);
+      }
     }
   }
   block_barrier();  // every wave is done with the stage buffers (reused below)
-  store_partials<JB, BR>(p, vg, row0, rbase, wv, hh, n, m_run, s_run, i_run, &lds_w[0][0]);
+  store_partials<JB, BR, SAMPLE>(p, vg, row0, rbase, wv, hh, n, m_run, s_run, i_run, g_best, g_id, &lds_w[0][0]);
 }
 
 // float32 path: one workgroup per (vocabulary group, row); plain FMA dot products.
@@ -427,10 +501,21 @@ __global__ __launch_bounds__(256) void slot_conf_f32_kernel(ConfParams p) {
   const int v_hi = (int)((long long)(vg + 1) * p.V / p.n_vg);
   float m = kNegBig, s = 0.f;
   int idx = INT_MAX;
+  float g = -INFINITY;  // sampling candidate
+  int gi = INT_MAX;
   for (int v = v_lo + tid; v < v_hi; v += 256) {
     const float* wr = W + (size_t)v * p.H;
     float z = 0.f;
     for (int k = 0; k < p.H; ++k) z = fmaf(hs[k], wr[k], z);
+    if (p.part_g) {
+      const uint4 r = philox4x32_10((uint32_t)v >> 2, (uint32_t)row, p.off_lo, p.off_hi, p.seed_lo, p.seed_hi);
+      const uint32_t words[4] = {r.x, r.y, r.z, r.w};
+      const float sc = fmaf(z, p.c2t, gumbel_log2(words[v & 3]));
+      if (sc > g) {
+        g = sc;
+        gi = v;
+      }
+    }
     if (z > m) {
       s = s * fast_exp2((m - z) * kLog2e) + 1.f;
       m = z;
@@ -442,9 +527,13 @@ __global__ __launch_bounds__(256) void slot_conf_f32_kernel(ConfParams p) {
   float* rm = hs + p.H;
   float* rs = rm + 256;
   int* ri = reinterpret_cast<int*>(rs + 256);
+  float* rg = reinterpret_cast<float*>(ri + 256);
+  int* rgi = reinterpret_cast<int*>(rg + 256);
   rm[tid] = m;
   rs[tid] = s;
   ri[tid] = idx;
+  rg[tid] = g;
+  rgi[tid] = gi;
   __syncthreads();
   for (int off = 128; off > 0; off >>= 1) {
     if (tid < off) {
@@ -454,6 +543,11 @@ __global__ __launch_bounds__(256) void slot_conf_f32_kernel(ConfParams p) {
       rm[tid] = a;
       rs[tid] = b;
       ri[tid] = c;
+      float g1 = rg[tid];
+      int i1 = rgi[tid];
+      sample_merge(g1, i1, rg[tid + off], rgi[tid + off]);
+      rg[tid] = g1;
+      rgi[tid] = i1;
     }
     __syncthreads();
   }
@@ -462,20 +556,46 @@ __global__ __launch_bounds__(256) void slot_conf_f32_kernel(ConfParams p) {
     p.part_m[o] = rm[0];
     p.part_s[o] = rs[0];
     p.part_idx[o] = ri[0];
+    if (p.part_g) {
+      p.part_g[o] = rg[0];
+      p.part_gi[o] = rgi[0];
+    }
   }
 }
 
-// Per row: merge the vocabulary-group partials in a fixed order and finish
-// max_prob = 1 / sum exp(x - max), lse and the target probability.
+// Logit of vocab id v for a row, hidden . w_vocab[v], as a float32 dot
+// product spread over the 64 lanes of a wave (every lane gets the sum).
+__device__ float row_logit(const ConfMergeParams& p, int row, int v, int lane) {
+  float z = 0.f;
+  if (p.bf16) {
+    const uint16_t* hr = static_cast<const uint16_t*>(p.hidden) + (size_t)row * p.H;
+    const uint16_t* wr = static_cast<const uint16_t*>(p.w_vocab) + (size_t)v * p.H;
+    for (int k = lane; k < p.H; k += 64) z = fmaf(bf16_to_f32(hr[k]), bf16_to_f32(wr[k]), z);
+  } else {
+    const float* hr = static_cast<const float*>(p.hidden) + (size_t)row * p.H;
+    const float* wr = static_cast<const float*>(p.w_vocab) + (size_t)v * p.H;
+    for (int k = lane; k < p.H; k += 64) z = fmaf(hr[k], wr[k], z);
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) z += __shfl_xor(z, off);
+  return z;
+}
+
+// Per row (one wave): merge the vocabulary-group partials in a fixed order
+// and finish max_prob = 1 / sum exp(x - max), lse, the target probability
+// and, when sampling, the sampled id and its probability.
 __global__ __launch_bounds__(256) void slot_conf_merge_kernel(ConfMergeParams p) {
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (row >= p.M) return;
   float m = kNegBig, s = 0.f;
   int idx = INT_MAX;
+  float sg = -INFINITY;
+  int sgi = INT_MAX;
   for (int g = lane; g < p.n_vg; g += 64) {
     const size_t o = (size_t)row * p.n_vg + g;  // a row's partials are contiguous
     stat_merge(m, s, idx, p.part_m[o], p.part_s[o], p.part_idx[o]);
+    if (p.part_g) sample_merge(sg, sgi, p.part_g[o], p.part_gi[o]);
   }
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) {
@@ -483,33 +603,27 @@ __global__ __launch_bounds__(256) void slot_conf_merge_kernel(ConfMergeParams p)
     const float s2 = __shfl_xor(s, off);
     const int i2 = __shfl_xor(idx, off);
     stat_merge(m, s, idx, m2, s2, i2);
+    if (p.part_g) {
+      const float g2 = __shfl_xor(sg, off);
+      const int gi2 = __shfl_xor(sgi, off);
+      sample_merge(sg, sgi, g2, gi2);
+    }
   }
   const float lse2 = m * kLog2e + __log2f(s);
-  float z = 0.f;
-  int tgt = -1;
-  if (p.target_ids) {
-    tgt = p.target_ids[row];
-    if (tgt >= 0 && tgt < p.V) {
-      if (p.bf16) {
-        const uint16_t* hr = static_cast<const uint16_t*>(p.hidden) + (size_t)row * p.H;
-        const uint16_t* wr = static_cast<const uint16_t*>(p.w_vocab) + (size_t)tgt * p.H;
-        for (int k = lane; k < p.H; k += 64) z = fmaf(bf16_to_f32(hr[k]), bf16_to_f32(wr[k]), z);
-      } else {
-        const float* hr = static_cast<const float*>(p.hidden) + (size_t)row * p.H;
-        const float* wr = static_cast<const float*>(p.w_vocab) + (size_t)tgt * p.H;
-        for (int k = lane; k < p.H; k += 64) z = fmaf(hr[k], wr[k], z);
-      }
-    }
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) z += __shfl_xor(z, off);
-  }
+  const int tgt = p.target_ids ? p.target_ids[row] : -1;
+  const bool tgt_ok = tgt >= 0 && tgt < p.V;
+  const float zt = tgt_ok ? row_logit(p, row, tgt, lane) : 0.f;
+  // every row has a finite perturbed score, so sgi is a valid id
+  const float zs = p.part_g ? row_logit(p, row, sgi, lane) : 0.f;
   if (lane != 0) return;
-  p.max_prob[row] = 1.f / s;
-  p.argmax_id[row] = idx;
+  if (p.max_prob) p.max_prob[row] = 1.f / s;
+  if (p.argmax_id) p.argmax_id[row] = idx;
   if (p.lse) p.lse[row] = lse2 * kLn2;
-  if (p.target_ids && p.target_prob) {
-    p.target_prob[row] = (tgt >= 0 && tgt < p.V) ? fast_exp2(z * kLog2e - lse2) : __builtin_nanf("");
+  if (p.part_g) {
+    p.sample_id[row] = sgi;
+    p.sample_prob[row] = fast_exp2(zs * kLog2e - lse2);
   }
+  if (p.target_ids && p.target_prob) p.target_prob[row] = tgt_ok ? fast_exp2(zt * kLog2e - lse2) : __builtin_nanf("");
 }
 
 // Tile configuration (measured on MI355X over the 0.6B/1.7B/4B LM-head
@@ -538,13 +652,18 @@ int conf_tile_rows() { return ZARYA_CONF_BR; }
 int conf_target_workgroups() { return ZARYA_CONF_WGS; }
 
 hipError_t launch_slot_conf_bf16(const ConfParams& p, hipStream_t stream) {
-  slot_conf_bf16_kernel<ZARYA_CONF_NW, ZARYA_CONF_BR, ZARYA_CONF_BK, ZARYA_CONF_NSW, ZARYA_CONF_NSX>
-      <<<dim3(8 * p.per_xcd), dim3(ZARYA_CONF_NW * 64), 0, stream>>>(p);
+  if (p.part_g) {
+    slot_conf_bf16_kernel<ZARYA_CONF_NW, ZARYA_CONF_BR, ZARYA_CONF_BK, ZARYA_CONF_NSW, ZARYA_CONF_NSX, true>
+        <<<dim3(8 * p.per_xcd), dim3(ZARYA_CONF_NW * 64), 0, stream>>>(p);
+  } else {
+    slot_conf_bf16_kernel<ZARYA_CONF_NW, ZARYA_CONF_BR, ZARYA_CONF_BK, ZARYA_CONF_NSW, ZARYA_CONF_NSX, false>
+        <<<dim3(8 * p.per_xcd), dim3(ZARYA_CONF_NW * 64), 0, stream>>>(p);
+  }
   return hipGetLastError();
 }
 
 hipError_t launch_slot_conf_f32(const ConfParams& p, hipStream_t stream) {
-  const size_t shm = (size_t)p.H * 4 + 256 * 12;
+  const size_t shm = (size_t)p.H * 4 + 256 * 20;
   hipLaunchKernelGGL(slot_conf_f32_kernel, dim3(p.n_vg, p.M), dim3(256), shm, stream, p);
   return hipGetLastError();
 }

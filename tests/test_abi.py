@@ -35,7 +35,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_version_and_status_strings():
     L = _lib.lib()
-    assert L.zarya_version() == 2
+    assert L.zarya_version() == 3
     for code, name in [(0, "ZARYA_OK"), (1, "ZARYA_ERR_INVALID_ARGUMENT"), (2, "ZARYA_ERR_UNSUPPORTED"),
                        (3, "ZARYA_ERR_WORKSPACE_TOO_SMALL"), (4, "ZARYA_ERR_HIP")]:
         assert L.zarya_status_string(code).decode() == name
@@ -127,6 +127,40 @@ def test_slot_confidence_workspace_checks():
     assert need >= 64 * 1024 * 12
     assert _conf_status(d, ws_bytes=need - 1) == _lib.ERR_WORKSPACE_TOO_SMALL
     assert _conf_status(d, ptr=0) == _lib.ERR_INVALID_ARGUMENT
+
+
+def _sample_status(desc, temperature=1.0, ptr=1, ws_bytes=1 << 40, params=True, out_null=None):
+    p = ctypes.c_void_p(ptr) if ptr else None
+    sp = _lib.SampleParams(temperature=temperature, seed=1, offset=2)
+    outs = [p, p]
+    if out_null is not None:
+        outs[out_null] = None
+    return _lib.lib().zarya_slot_sample(ctypes.byref(desc), ctypes.byref(sp) if params else None, p, p, *outs,
+                                        None, None, p, ws_bytes, None)
+
+
+@pytest.mark.parametrize("temperature", [0.0, -1.0, float("nan"), float("inf"), 1e-31])
+def test_slot_sample_rejects_bad_temperatures(temperature):
+    d = _lib.ConfDesc(n_rows=64, hidden=1024, vocab=151936, dtype=1)
+    assert _sample_status(d, temperature=temperature) == _lib.ERR_INVALID_ARGUMENT
+    assert "temperature" in _lib.lib().zarya_last_error().decode()
+
+
+def test_slot_sample_argument_checks():
+    d = _lib.ConfDesc(n_rows=1024, hidden=1024, vocab=151936, dtype=1)
+    need = _lib.slot_sample_workspace_size(d)
+    # two more partial arrays than the greedy reduction: best perturbed score and its id
+    assert need > _lib.slot_confidence_workspace_size(d)
+    assert need >= 64 * 1024 * 20
+    assert _sample_status(d, ws_bytes=need - 1) == _lib.ERR_WORKSPACE_TOO_SMALL
+    assert _sample_status(d, ptr=0) == _lib.ERR_INVALID_ARGUMENT
+    assert _sample_status(d, params=False) == _lib.ERR_INVALID_ARGUMENT
+    assert _sample_status(d, out_null=0) == _lib.ERR_INVALID_ARGUMENT  # sample_id is required
+    assert _sample_status(d, out_null=1) == _lib.ERR_INVALID_ARGUMENT  # sample_prob is required
+    for bad, code in [(dict(n_rows=0), _lib.ERR_INVALID_ARGUMENT), (dict(hidden=1001), _lib.ERR_UNSUPPORTED)]:
+        base = dict(n_rows=64, hidden=1024, vocab=151936, dtype=1)
+        base.update(bad)
+        assert _sample_status(_lib.ConfDesc(**base)) == code
 
 
 @pytest.mark.parametrize("args,code", [
