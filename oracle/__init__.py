@@ -21,6 +21,8 @@ Language Model with Flexible Training and Dual-Mode Inference"):
 * ``verify``      -- token acceptance after the verification pass and the
   KV-cache append of the accepted tokens (Sec. 5.2 "Verification phase",
   "KV cache update").
+* ``mdm``         -- Mode A: the mask budget of a generation and the positions
+  revealed at a denoising step (Sec. 5.1 steps 1-3).
 
 Every function is the plain definition written out in float64 numpy; there is
 no blocking, fusion or reordering beyond what the definition states.
@@ -48,6 +50,7 @@ from .selection import (
 
 from .sampling import gumbel, philox4x32, slot_sample, uniforms
 from .verify import ACCEPT_PREFIX, ACCEPT_PER_TOKEN, accept_tokens, kv_append
+from .mdm import REVEAL_CONFIDENCE, REVEAL_LEFTMOST, REVEAL_RANDOM, mask_budget, reveal
 
 __all__ = [
     "PASS_DIFFUSION",
@@ -74,4 +77,9 @@ __all__ = [
     "uniforms",
     "gumbel",
     "slot_sample",
+    "REVEAL_CONFIDENCE",
+    "REVEAL_LEFTMOST",
+    "REVEAL_RANDOM",
+    "mask_budget",
+    "reveal",
 ]

@@ -589,3 +589,142 @@ def check_sampling_cold_and_prob(sample):
 PHILOX_CHECKS = [check_philox_kat]
 UNIFORM_CHECKS = [check_uniform_moments, check_gumbel_moments]
 SAMPLING_CHECKS = [check_sampling_distribution, check_sampling_cold_and_prob]
+
+
+# ---------------------------------------------------------------- Mode A (Sec. 5.1)
+
+def load_mdm_golden():
+    with open(os.path.join(GOLDEN, "mdm_cases.json")) as f:
+        return json.load(f)
+
+
+def check_budget_golden(budget):
+    """Hand cases of the mask budget (Sec. 5.1 step 1 and its readings)."""
+    for case in load_mdm_golden()["budget"]:
+        counts, t = budget(case["n_masked"], case["n_steps"], case["alpha0"], seed=3)
+        assert list(map(int, counts)) == case["expect"], f"{case['name']}: got {list(counts)}"
+        assert t == case["n_diffusion_steps"], f"{case['name']}: {t} diffusion steps"
+
+
+def check_budget_structure(budget):
+    """Every plan reveals each mask exactly once; diffusion steps are as even
+    as possible; sequential steps reveal one token; T = 0 gives steps of at
+    most four."""
+    rng = np.random.default_rng(80)
+    for _ in range(200):
+        N = int(rng.integers(0, 300))
+        T = int(rng.integers(0, 12))
+        a = float(rng.choice([0.0, 0.1, 0.25, 0.5, 0.9, 1.0]))
+        counts, t = budget(N, T, a, seed=int(rng.integers(0, 2**63)))
+        counts = np.asarray(counts)
+        assert counts.sum() == N, (N, T, a)
+        if N == 0:
+            assert counts.size == 0 and t == 0
+            continue
+        assert t == (T if T > 0 else -(-N // 4))
+        diff, seq = counts[:t], counts[t:]
+        assert diff.size == t and np.all(seq == 1)
+        assert diff.max() - diff.min() <= 1 and np.all(np.diff(diff) <= 0)
+        if T == 0:
+            assert seq.size == 0 and diff.max() <= 4
+        if T > 0 and a == 0.0:  # T = 0 skips the binomial draw
+            assert diff.sum() == 0
+        if a == 1.0:
+            assert seq.size == 0
+
+
+def check_budget_binomial(budget):
+    """The number of diffusion tokens follows Binomial(N, alpha_0) over seeds
+    (chi-square against scipy's pmf, bins with expectation >= 5)."""
+    import scipy.stats
+
+    N, a, runs = 40, 0.3, 4000
+    n_diff = np.array([int(np.asarray(budget(N, 5, a, seed=s)[0])[:5].sum()) for s in range(runs)])
+    obs = np.bincount(n_diff, minlength=N + 1).astype(np.float64)
+    exp = scipy.stats.binom.pmf(np.arange(N + 1), N, a) * runs
+    keep = exp >= 5
+    o = np.append(obs[keep], obs[~keep].sum())
+    e = np.append(exp[keep], exp[~keep].sum())
+    chi2 = float(((o - e) ** 2 / e).sum())
+    assert chi2 < scipy.stats.chi2.ppf(1 - 1e-4, o.size - 1), f"chi2 {chi2:.1f} over {o.size - 1} dof"
+    assert abs(n_diff.mean() - N * a) < 5 * np.sqrt(N * a * (1 - a) / runs)
+
+
+def _reveal_conf(values):
+    return np.array([np.nan if v == "nan" else v for v in values], dtype=np.float32)
+
+
+def check_reveal_golden(reveal):
+    """Hand cases of the reveal rules."""
+    for case in load_mdm_golden()["reveal"]:
+        conf = _reveal_conf(case["conf"])[None]
+        op = np.array(case["open"], dtype=bool)[None]
+        order, n, op2, _ = reveal(conf, op, [case["k"]], case["rule"])
+        exp = case["expect"]
+        assert order[0, : len(exp)].tolist() == exp and np.all(order[0, len(exp):] == -1), \
+            f"{case['name']}: got {order[0].tolist()}"
+        assert int(n[0]) == len(exp)
+        want = op[0].copy()
+        want[exp] = False
+        assert np.array_equal(op2[0], want), f"{case['name']}: open mask"
+
+
+def check_reveal_invariants(reveal):
+    """Random rows, all three rules: revealed positions were open and are now
+    closed, n = min(k, open count), tokens change only there; the confidence
+    rule matches a stable descending sort of the open positions, the leftmost
+    rule the lowest open indices."""
+    rng = np.random.default_rng(81)
+    B, N = 30, 17
+    conf = rng.random((B, N)).astype(np.float32)
+    conf[rng.random((B, N)) < 0.2] = np.float32(0.5)  # ties
+    op = rng.random((B, N)) < 0.7
+    k = rng.integers(0, N + 3, B)
+    tokens = rng.integers(0, 1000, (B, N))
+    sid = rng.integers(0, 1000, (B, N))
+    for rule in (oracle.REVEAL_CONFIDENCE, oracle.REVEAL_LEFTMOST, oracle.REVEAL_RANDOM):
+        order, n, op2, tok = reveal(conf, op, k, rule, seed=5, offset=6, tokens=tokens, sample_id=sid)
+        for b in range(B):
+            cnt = int(n[b])
+            opened = np.flatnonzero(op[b])
+            assert cnt == min(int(k[b]), opened.size)
+            pick = order[b, :cnt]
+            assert np.all(order[b, cnt:] == -1) and len(set(pick.tolist())) == cnt
+            assert np.all(op[b, pick]) and not np.any(op2[b, pick])
+            assert np.array_equal(op2[b] | np.isin(np.arange(N), pick), op[b])
+            assert np.array_equal(tok[b, pick], sid[b, pick])
+            rest = np.setdiff1d(np.arange(N), pick)
+            assert np.array_equal(tok[b, rest], tokens[b, rest])
+            if rule == oracle.REVEAL_CONFIDENCE:
+                ranked = opened[np.argsort(-conf[b, opened].astype(np.float64), kind="stable")]
+                assert np.array_equal(pick, ranked[:cnt])
+            if rule == oracle.REVEAL_LEFTMOST:
+                assert np.array_equal(pick, opened[:cnt])
+
+
+def check_reveal_random_uniform(reveal):
+    """REVEAL_RANDOM chooses a uniformly random subset: over many offsets each
+    open position is revealed with probability k / #open and is the first
+    pick with probability 1 / #open; batch rows draw independently."""
+    N, k, runs = 6, 2, 3000
+    op = np.ones((2, N), dtype=bool)
+    op[:, 4] = False  # 5 open positions
+    hits = np.zeros(N)
+    first = np.zeros(N)
+    same = 0
+    for off in range(runs):
+        order, n, _, _ = reveal(np.zeros((2, N), np.float32), op, [k, k], oracle.REVEAL_RANDOM, seed=9, offset=off)
+        hits[order[0, :k]] += 1
+        first[order[0, 0]] += 1
+        same += int(set(order[0, :k].tolist()) == set(order[1, :k].tolist()))
+    assert hits[4] == 0 and first[4] == 0
+    p = k / 5
+    assert np.all(np.abs(hits[op[0]] / runs - p) < 5 * np.sqrt(p * (1 - p) / runs)), hits
+    q = 1 / 5
+    assert np.all(np.abs(first[op[0]] / runs - q) < 5 * np.sqrt(q * (1 - q) / runs)), first
+    # two rows agree on the subset with probability 1 / C(5, 2) = 0.1
+    assert abs(same / runs - 0.1) < 5 * np.sqrt(0.09 / runs), same
+
+
+BUDGET_CHECKS = [check_budget_golden, check_budget_structure, check_budget_binomial]
+REVEAL_CHECKS = [check_reveal_golden, check_reveal_invariants, check_reveal_random_uniform]

@@ -421,3 +421,116 @@ def test_uniform_mutant_is_caught(name):
 @pytest.mark.parametrize("name", list(SAMPLING_MUTANTS))
 def test_sampling_mutant_is_caught(name):
     assert _caught(SAMPLING_MUTANTS[name], pins.SAMPLING_CHECKS), f"mutant '{name}' passed every pin"
+
+
+import oracle.mdm as omd  # noqa: E402
+
+
+def _budget_t0_rounds_down(N, T, a, seed):
+    if T == 0 and N > 0:
+        t = max(1, N // 4)
+        base, extra = divmod(N, t)
+        return np.array([base + (1 if i < extra else 0) for i in range(t)]), t
+    return omd.mask_budget(N, T, a, seed)
+
+
+def _budget_drops_sequential(N, T, a, seed):
+    counts, t = omd.mask_budget(N, T, a, seed)
+    return counts[:t], t
+
+
+def _budget_complement(N, T, a, seed):
+    return omd.mask_budget(N, T, 1.0 - a if T > 0 else a, seed)
+
+
+def _budget_extra_last(N, T, a, seed):
+    counts, t = omd.mask_budget(N, T, a, seed)
+    return np.concatenate([counts[:t][::-1], counts[t:]]), t
+
+
+def _budget_t0_binomial(N, T, a, seed):
+    if T == 0 and N > 0:
+        return omd.mask_budget(N, -(-N // 4), a, seed)
+    return omd.mask_budget(N, T, a, seed)
+
+
+BUDGET_MUTANTS = {
+    "T = 0 rounds the step count down": _budget_t0_rounds_down,
+    "sequential tokens dropped": _budget_drops_sequential,
+    "binomial with 1 - alpha_0": _budget_complement,
+    "extra tokens to the last steps": _budget_extra_last,
+    "T = 0 still draws the binomial": _budget_t0_binomial,
+}
+
+
+def _rev_ties_high(conf, op, k, rule=0, seed=0, offset=0, tokens=None, sample_id=None):
+    if rule != omd.REVEAL_CONFIDENCE:
+        return omd.reveal(conf, op, k, rule, seed, offset, tokens, sample_id)
+    c = np.asarray(conf, np.float32)
+    N = c.shape[1]
+    # reverse the positions, so equal confidences favour the higher index
+    o, n, op2, tok = omd.reveal(c[:, ::-1], np.asarray(op)[:, ::-1], k, rule, seed, offset)
+    o = np.where(o >= 0, N - 1 - o, -1).astype(np.int32)
+    tok2 = None
+    if tokens is not None:
+        tok2 = np.array(tokens, copy=True)
+        for b in range(c.shape[0]):
+            for i in o[b, : n[b]]:
+                tok2[b, i] = sample_id[b][i]
+    return o, n, op2[:, ::-1], tok2
+
+
+def _rev_lowest_first(conf, op, k, rule=0, seed=0, offset=0, tokens=None, sample_id=None):
+    c = np.asarray(conf, np.float32)
+    return omd.reveal(-c if rule == omd.REVEAL_CONFIDENCE else c, op, k, rule, seed, offset, tokens, sample_id)
+
+
+def _rev_ignores_open(conf, op, k, rule=0, seed=0, offset=0, tokens=None, sample_id=None):
+    o, n, _, tok = omd.reveal(conf, np.ones_like(np.asarray(op, bool)), k, rule, seed, offset, tokens, sample_id)
+    op2 = np.asarray(op, bool).copy()
+    for b in range(op2.shape[0]):
+        op2[b, o[b, : n[b]]] = False
+    return o, n, op2, tok
+
+
+def _rev_rightmost(conf, op, k, rule=0, seed=0, offset=0, tokens=None, sample_id=None):
+    if rule != omd.REVEAL_LEFTMOST:
+        return omd.reveal(conf, op, k, rule, seed, offset, tokens, sample_id)
+    N = np.asarray(op).shape[1]
+    return omd.reveal(np.tile(np.arange(N, dtype=np.float32), (np.asarray(op).shape[0], 1)), op, k,
+                      omd.REVEAL_CONFIDENCE, seed, offset, tokens, sample_id)
+
+
+def _rev_random_row_ignored(conf, op, k, rule=0, seed=0, offset=0, tokens=None, sample_id=None):
+    if rule != omd.REVEAL_RANDOM:
+        return omd.reveal(conf, op, k, rule, seed, offset, tokens, sample_id)
+    saved = omd.uniforms
+    omd.uniforms = lambda rows, vocab, s, o: saved([0] * len(np.ravel(rows)), vocab, s, o)
+    try:
+        return omd.reveal(conf, op, k, rule, seed, offset, tokens, sample_id)
+    finally:
+        omd.uniforms = saved
+
+
+def _rev_random_offset_ignored(conf, op, k, rule=0, seed=0, offset=0, tokens=None, sample_id=None):
+    return omd.reveal(conf, op, k, rule, seed, 0, tokens, sample_id)
+
+
+REVEAL_MUTANTS = {
+    "confidence ties to the higher index": _rev_ties_high,
+    "lowest confidence first": _rev_lowest_first,
+    "open mask ignored": _rev_ignores_open,
+    "sequential phase from the right": _rev_rightmost,
+    "random choice not keyed by row": _rev_random_row_ignored,
+    "random choice ignores the step offset": _rev_random_offset_ignored,
+}
+
+
+@pytest.mark.parametrize("name", list(BUDGET_MUTANTS))
+def test_budget_mutant_is_caught(name):
+    assert _caught(BUDGET_MUTANTS[name], pins.BUDGET_CHECKS), f"mutant '{name}' passed every pin"
+
+
+@pytest.mark.parametrize("name", list(REVEAL_MUTANTS))
+def test_reveal_mutant_is_caught(name):
+    assert _caught(REVEAL_MUTANTS[name], pins.REVEAL_CHECKS), f"mutant '{name}' passed every pin"

@@ -96,3 +96,13 @@ def test_uniform_pin(check):
 @pytest.mark.parametrize("check", pins.SAMPLING_CHECKS, ids=lambda f: f.__name__)
 def test_sampling_pin(check):
     check(oracle.slot_sample)
+
+
+@pytest.mark.parametrize("check", pins.BUDGET_CHECKS, ids=lambda f: f.__name__)
+def test_budget_pin(check):
+    check(oracle.mask_budget)
+
+
+@pytest.mark.parametrize("check", pins.REVEAL_CHECKS, ids=lambda f: f.__name__)
+def test_reveal_pin(check):
+    check(oracle.reveal)
