@@ -29,6 +29,15 @@
  *   6. zarya_slot_sample      Gumbel-max sampling fused into the LM-head
  *                             reduction of 2.
  *
+ * Mode A, MDM sampling with first-hitting denoising (Sec. 5.1), runs the same
+ * kernels on a masked tail (zarya_slot_attn with slot_len 1 and cross_slot
+ * CAUSAL, then zarya_slot_sample) plus
+ *
+ *   7. zarya_mdm_budget       host-side plan of how many masks each step
+ *                             reveals (Sec. 5.1 step 1);
+ *   8. zarya_mdm_reveal       the positions revealed at a step, their tokens
+ *                             written and their mask flags cleared.
+ *
  * Conventions for every entry point:
  *  - Tensor arguments are DEVICE pointers to dense row-major (C-contiguous)
  *    arrays whose shapes are given in the comments; the caller owns every
@@ -58,7 +67,7 @@ extern "C" {
 #endif
 
 #define ZARYA_VERSION_MAJOR 0
-#define ZARYA_VERSION_MINOR 3
+#define ZARYA_VERSION_MINOR 4
 
 typedef enum zarya_status {
   ZARYA_OK = 0,
@@ -324,6 +333,63 @@ zarya_status zarya_slot_sample_workspace_size(const zarya_conf_desc* desc, size_
 zarya_status zarya_slot_sample(const zarya_conf_desc* desc, const zarya_sample_params* params, const void* hidden,
                                const void* w_vocab, int32_t* sample_id, float* sample_prob, float* max_prob,
                                float* lse, void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* 7. Mode A: mask budget (host)                                             */
+/* ------------------------------------------------------------------------ */
+/*
+ * Sec. 5.1 step 1 "Mask budget planning" for a generation with n_masked masks.
+ * n_steps T > 0: n_diff ~ Binomial(n_masked, alpha0) tokens go through exactly
+ * T diffusion steps, spread as evenly as possible (the first n_diff mod T
+ * steps take one more; steps may reveal 0), then n_masked - n_diff sequential
+ * steps reveal one token each.  T = 0: the binomial draw is skipped, T =
+ * ceil(n_masked / 4) and every token goes through diffusion.  The binomial
+ * draw counts the i < n_masked with u_i < alpha0 (in double), u_i the uniform
+ * of row 0, id i, offset 0 of the Philox stream of zarya_slot_sample under
+ * key `seed`.
+ *
+ * counts             HOST int32 [capacity] out: tokens revealed per step,
+ *                    diffusion steps first; NULL only asks for the length
+ * n_plan_steps       HOST out: number of steps of the plan (required)
+ * n_diffusion_steps  HOST out or NULL
+ * Requires n_masked >= 0, n_steps >= 0, 0 <= alpha0 <= 1, capacity >= the plan
+ * length when counts is given.  Runs on the host only; touches no device.
+ */
+zarya_status zarya_mdm_budget(int32_t n_masked, int32_t n_steps, double alpha0, uint64_t seed, int32_t* counts,
+                              int32_t capacity, int32_t* n_plan_steps, int32_t* n_diffusion_steps);
+
+/* ------------------------------------------------------------------------ */
+/* 8. Mode A: positions revealed at a denoising step                         */
+/* ------------------------------------------------------------------------ */
+typedef enum zarya_reveal_rule {
+  ZARYA_REVEAL_CONFIDENCE = 0, /* the k most confident open positions: descending conf,
+                                  ties to the lower index, NaN as -inf                   */
+  ZARYA_REVEAL_LEFTMOST = 1,   /* the k lowest open positions (sequential phase)          */
+  ZARYA_REVEAL_RANDOM = 2      /* a uniformly random k-subset (first-hitting sampler): the
+                                  k smallest uniforms u(b, pos) of the zarya_slot_sample
+                                  stream (row b, id pos) under seed/offset, ties to the
+                                  lower index                                            */
+} zarya_reveal_rule;
+
+/*
+ * For each batch row b, reveal min(k[b], open count) of the N positions whose
+ * mask flag is set (Sec. 5.1 steps 2-3: revealed tokens join the committed part
+ * of the sequence, the rest stay masked).
+ *
+ * conf       [B, N] float32     confidence of each position's drawn token
+ *                               (sample_prob); used by CONFIDENCE, else may be NULL
+ * mask       [B, N] uint8 in/out  nonzero = still masked; cleared where revealed
+ * k          [B] int32          tokens to reveal in row b (negative counts as 0)
+ * sample_id  [B, N] int32 or NULL  drawn token of each position
+ * tokens     [B, N] int32 in/out or NULL  receives sample_id at revealed
+ *                               positions (both or neither of the two)
+ * order      [B, N] int32 out   revealed positions in reveal order, then -1
+ * n_revealed [B] int32 out or NULL
+ * Requires 1 <= N <= 8192.  Integer work: bit-identical to the rule.
+ */
+zarya_status zarya_mdm_reveal(int32_t batch, int32_t n, const float* conf, uint8_t* mask, const int32_t* k,
+                              int32_t rule, uint64_t seed, uint64_t offset, const int32_t* sample_id, int32_t* tokens,
+                              int32_t* order, int32_t* n_revealed, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
 /* Diagnostics                                                               */

@@ -35,6 +35,9 @@ from ._lib import (  # noqa: F401
     DTYPE_F32,
     PASS_AR_INFILL,
     PASS_DIFFUSION,
+    REVEAL_CONFIDENCE,
+    REVEAL_LEFTMOST,
+    REVEAL_RANDOM,
     SELECT_THRESHOLD,
     SELECT_TOP_K,
     SLOT_CONF_FIRST_TOKEN,
@@ -47,6 +50,11 @@ __all__ = [
     "slot_attn_desc",
     "slot_confidence",
     "slot_sample",
+    "mdm_budget",
+    "mdm_reveal",
+    "REVEAL_CONFIDENCE",
+    "REVEAL_LEFTMOST",
+    "REVEAL_RANDOM",
     "select_slots",
     "verify_accept",
     "kv_append",
@@ -201,6 +209,45 @@ def slot_sample(hidden, w_vocab, temperature, seed, offset=0, out=None, workspac
         _ptr(out["sample_prob"]), _ptr(out.get("max_prob")), _ptr(out.get("lse")), _ptr(workspace),
         workspace.numel(), _stream()))
     return out
+
+
+def mdm_budget(n_masked, n_steps, alpha0, seed):
+    """Mode A mask budget (host): (counts per step, number of diffusion steps)."""
+    L = _lib.lib()
+    n, t = ctypes.c_int32(0), ctypes.c_int32(0)
+    args = (int(n_masked), int(n_steps), float(alpha0), int(seed) & (2**64 - 1))
+    _lib.check(L.zarya_mdm_budget(*args, None, 0, ctypes.byref(n), ctypes.byref(t)))
+    counts = (ctypes.c_int32 * max(1, n.value))()
+    _lib.check(L.zarya_mdm_budget(*args, counts, n.value, ctypes.byref(n), ctypes.byref(t)))
+    return [int(c) for c in counts[: n.value]], t.value
+
+
+def mdm_reveal(mask, k, rule=REVEAL_CONFIDENCE, conf=None, seed=0, offset=0, sample_id=None, tokens=None,
+               out=None):
+    """Reveal positions of a Mode A step.
+
+    mask [B,N] uint8 (nonzero = masked; cleared where revealed, in place),
+    k [B] int32, conf [B,N] float32 (confidence rule), sample_id / tokens
+    [B,N] int32 (optional pair; tokens updated in place).
+    Returns (order [B,N] int32: revealed positions then -1, n_revealed [B] int32).
+    """
+    B, N = mask.shape
+    dev = mask.device
+    _need(mask, "mask", (B, N), torch.uint8, dev)
+    _need(k, "k", (B,), torch.int32, dev)
+    if conf is not None:
+        _need(conf, "conf", (B, N), torch.float32, dev)
+    if sample_id is not None:
+        _need(sample_id, "sample_id", (B, N), torch.int32, dev)
+    if tokens is not None:
+        _need(tokens, "tokens", (B, N), torch.int32, dev)
+    if out is None:
+        out = (torch.empty((B, N), dtype=torch.int32, device=dev), torch.empty((B,), dtype=torch.int32, device=dev))
+    order, n = out
+    _lib.check(_lib.lib().zarya_mdm_reveal(
+        B, N, _ptr(conf), _ptr(mask), _ptr(k), int(rule), int(seed) & (2**64 - 1), int(offset) & (2**64 - 1),
+        _ptr(sample_id), _ptr(tokens), _ptr(order), _ptr(n), _stream()))
+    return order, n
 
 
 def select_slots(token_conf, slot_open=None, conf_rule=SLOT_CONF_FIRST_TOKEN, rule=SELECT_THRESHOLD,

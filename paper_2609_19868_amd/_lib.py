@@ -32,6 +32,9 @@ SELECT_THRESHOLD = 0
 SELECT_TOP_K = 1
 ACCEPT_PREFIX = 0
 ACCEPT_PER_TOKEN = 1
+REVEAL_CONFIDENCE = 0
+REVEAL_LEFTMOST = 1
+REVEAL_RANDOM = 2
 
 # every symbol include/zarya.h declares
 EXPORTS = (
@@ -44,6 +47,8 @@ EXPORTS = (
     "zarya_kv_append",
     "zarya_slot_sample_workspace_size",
     "zarya_slot_sample",
+    "zarya_mdm_budget",
+    "zarya_mdm_reveal",
     "zarya_status_string",
     "zarya_last_error",
     "zarya_version",
@@ -136,6 +141,11 @@ def lib():
         L.zarya_slot_sample.argtypes = [ctypes.POINTER(ConfDesc), ctypes.POINTER(SampleParams), vp, vp, vp, vp, vp,
                                         vp, vp, sz, vp]
         L.zarya_slot_sample.restype = ctypes.c_int
+        u64, ip = ctypes.c_uint64, ctypes.POINTER(i32)
+        L.zarya_mdm_budget.argtypes = [i32, i32, ctypes.c_double, u64, ip, i32, ip, ip]
+        L.zarya_mdm_budget.restype = ctypes.c_int
+        L.zarya_mdm_reveal.argtypes = [i32, i32, vp, vp, vp, i32, u64, u64, vp, vp, vp, vp, vp]
+        L.zarya_mdm_reveal.restype = ctypes.c_int
         L.zarya_status_string.argtypes = [ctypes.c_int]
         L.zarya_status_string.restype = ctypes.c_char_p
         L.zarya_last_error.argtypes = []

@@ -379,6 +379,59 @@ zarya_status zarya_slot_sample(const zarya_conf_desc* d, const zarya_sample_para
                   stream);
 }
 
+zarya_status zarya_mdm_budget(int32_t n_masked, int32_t n_steps, double alpha0, uint64_t seed, int32_t* counts,
+                              int32_t capacity, int32_t* n_plan_steps, int32_t* n_diffusion_steps) {
+  if (n_masked < 0 || n_steps < 0)
+    return fail(ZARYA_ERR_INVALID_ARGUMENT, "n_masked (%d) and n_steps (%d) must be >= 0", n_masked, n_steps);
+  if (!(alpha0 >= 0.0 && alpha0 <= 1.0)) return fail(ZARYA_ERR_INVALID_ARGUMENT, "alpha0 %g is not in [0, 1]", alpha0);
+  if (!n_plan_steps) return fail(ZARYA_ERR_INVALID_ARGUMENT, "n_plan_steps is NULL");
+  int32_t t = 0;
+  const int64_t len = mask_budget_plan(n_masked, n_steps, alpha0, seed, nullptr, &t);
+  if (len > kI32Max) return fail(ZARYA_ERR_UNSUPPORTED, "plan of %lld steps", (long long)len);
+  if (counts) {
+    if (capacity < len)
+      return fail(ZARYA_ERR_INVALID_ARGUMENT, "counts holds %d steps, the plan has %lld", capacity, (long long)len);
+    mask_budget_plan(n_masked, n_steps, alpha0, seed, counts, &t);
+  }
+  *n_plan_steps = (int32_t)len;
+  if (n_diffusion_steps) *n_diffusion_steps = t;
+  return ZARYA_OK;
+}
+
+zarya_status zarya_mdm_reveal(int32_t batch, int32_t n, const float* conf, uint8_t* mask, const int32_t* k,
+                              int32_t rule, uint64_t seed, uint64_t offset, const int32_t* sample_id, int32_t* tokens,
+                              int32_t* order, int32_t* n_revealed, hipStream_t stream) {
+  if (batch < 1 || n < 1) return fail(ZARYA_ERR_INVALID_ARGUMENT, "batch and n must be >= 1");
+  if (n > kRevealMaxN) return fail(ZARYA_ERR_UNSUPPORTED, "n %d exceeds %d", n, kRevealMaxN);
+  if (rule != ZARYA_REVEAL_CONFIDENCE && rule != ZARYA_REVEAL_LEFTMOST && rule != ZARYA_REVEAL_RANDOM)
+    return fail(ZARYA_ERR_INVALID_ARGUMENT, "unknown reveal rule %d", rule);
+  if (!mask || !k || !order) return fail(ZARYA_ERR_INVALID_ARGUMENT, "mask, k and order are required");
+  if (rule == ZARYA_REVEAL_CONFIDENCE && !conf)
+    return fail(ZARYA_ERR_INVALID_ARGUMENT, "the confidence rule needs conf");
+  if ((tokens == nullptr) != (sample_id == nullptr))
+    return fail(ZARYA_ERR_INVALID_ARGUMENT, "tokens and sample_id go together");
+  if ((int64_t)batch * n > kI32Max) return fail(ZARYA_ERR_UNSUPPORTED, "batch * n exceeds 2^31");
+  (void)hipGetLastError();
+  RevealParams p{};
+  p.B = batch;
+  p.N = n;
+  p.NP = 2;
+  while (p.NP < n) p.NP <<= 1;
+  p.rule = rule;
+  p.conf = conf;
+  p.mask = mask;
+  p.k = k;
+  p.seed_lo = (uint32_t)seed;
+  p.seed_hi = (uint32_t)(seed >> 32);
+  p.off_lo = (uint32_t)offset;
+  p.off_hi = (uint32_t)(offset >> 32);
+  p.sample_id = sample_id;
+  p.tokens = tokens;
+  p.order = order;
+  p.n_revealed = n_revealed;
+  return hip_status(launch_mdm_reveal(p, stream), "mdm_reveal launch");
+}
+
 zarya_status zarya_select_slots(int32_t batch, int32_t n_slots, int32_t slot_len, const float* token_conf,
                                 const uint8_t* slot_open, int32_t conf_rule, int32_t rule, float threshold, int32_t k,
                                 float* slot_conf, int32_t* selected, int32_t* n_selected, hipStream_t stream) {

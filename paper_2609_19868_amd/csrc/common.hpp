@@ -111,8 +111,8 @@ __device__ __forceinline__ float max3f(float a, float b, float c) {
 // a 128-bit counter and a 64-bit key.  Each round multiplies counter words 0
 // and 2 by the two round constants, swaps the halves of the products into the
 // other words under the round key, and bumps the key by the two Weyl constants.
-__device__ __forceinline__ uint4 philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3, uint32_t k0,
-                                               uint32_t k1) {
+__host__ __device__ __forceinline__ uint4 philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3,
+                                                        uint32_t k0, uint32_t k1) {
 #pragma unroll
   for (int r = 0; r < 10; ++r) {
     const uint64_t p0 = (uint64_t)0xD2511F53u * c0;

@@ -118,6 +118,26 @@ struct AppendParams {
   void* v_cache;
 };
 
+// Mode A reveal: one workgroup per batch row sorts the row's N keys in LDS.
+struct RevealParams {
+  int B, N, NP;  // NP = N rounded up to a power of two (>= 2)
+  int rule;      // 0 confidence, 1 leftmost, 2 random
+  const float* conf;
+  uint8_t* mask;
+  const int32_t* k;
+  uint32_t seed_lo, seed_hi, off_lo, off_hi;
+  const int32_t* sample_id;
+  int32_t* tokens;
+  int32_t* order;
+  int32_t* n_revealed;
+};
+constexpr int kRevealMaxN = 8192;
+
+// Mode A mask budget on the host: fills counts (if not null) and returns the
+// plan length; *n_diff_steps gets the number of diffusion steps.
+int64_t mask_budget_plan(int32_t n_masked, int32_t n_steps, double alpha0, uint64_t seed, int32_t* counts,
+                         int32_t* n_diff_steps);
+
 // largest S*L the append kernel stages in LDS
 constexpr int kAppendMaxTokens = 8192;
 
@@ -136,5 +156,6 @@ hipError_t launch_slot_conf_merge(const ConfMergeParams& p, hipStream_t stream);
 hipError_t launch_select_slots(const SelectParams& p, hipStream_t stream);
 hipError_t launch_verify_accept(const AcceptParams& p, hipStream_t stream);
 hipError_t launch_kv_append(const AppendParams& p, hipStream_t stream);
+hipError_t launch_mdm_reveal(const RevealParams& p, hipStream_t stream);
 
 }  // namespace zarya

@@ -1,0 +1,140 @@
+// Mode A of Zarya (MDM sampling with first-hitting denoising, Sec. 5.1):
+// the mask budget of a generation (host) and the positions a denoising step
+// reveals (gfx950).
+//
+// What is computed (Sec. 5.1 steps 1-3): a generation with N masks runs T
+// diffusion steps that together reveal a Binomial(N, alpha_0) share of the
+// masks, then reveals the rest one per step; with T = 0 the draw is skipped
+// and T is a quarter of N.  At each step the model's drawn tokens of some
+// masked positions are committed -- the most confident ones, the leftmost ones
+// (sequential phase) or a uniformly random set (the first-hitting sampler) --
+// and those positions join the committed part of the sequence.
+//
+// The reveal is integer work on at most 8192 positions per row: each key packs
+// the rule's ordering (confidence, position, or a Philox uniform) above the
+// position, so one ascending bitonic sort in LDS yields the reveal order with
+// ties broken by the lower position.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace zarya {
+
+namespace {
+
+constexpr int kThreads = 1024;
+constexpr uint64_t kClosed = ~0ull;  // sorts after every open position
+
+// Float32 confidence -> 32-bit key that increases as the confidence falls
+// (NaN counts as -inf, -0 as +0), by integer operations only.
+__device__ __forceinline__ uint32_t conf_desc_key(float c) {
+  uint32_t b = __float_as_uint(c);
+  if ((b & 0x7F800000u) == 0x7F800000u && (b & 0x007FFFFFu) != 0) b = 0xFF800000u;  // NaN -> -inf
+  if (b == 0x80000000u) b = 0;                                                        // -0 -> +0
+  const uint32_t asc = (b & 0x80000000u) ? ~b : (b | 0x80000000u);  // increases with the value
+  return ~asc;
+}
+
+// Philox uniform of (row, position) as its 23-bit integer (x >> 9): the same
+// order as u = ((x >> 9) + 1/2) * 2^-23.
+__device__ __forceinline__ uint32_t uniform_bits(const RevealParams& p, int row, int pos) {
+  const uint4 r = philox4x32_10((uint32_t)pos >> 2, (uint32_t)row, p.off_lo, p.off_hi, p.seed_lo, p.seed_hi);
+  const uint32_t w[4] = {r.x, r.y, r.z, r.w};
+  return w[pos & 3] >> 9;
+}
+
+}  // namespace
+
+__global__ __launch_bounds__(kThreads) void mdm_reveal_kernel(RevealParams p) {
+  __shared__ uint64_t keys[kRevealMaxN];
+  __shared__ int n_open;
+  const int b = blockIdx.x;
+  const int tid = threadIdx.x;
+  const size_t base = (size_t)b * p.N;
+  if (tid == 0) n_open = 0;
+  __syncthreads();
+  int mine = 0;
+  for (int i = tid; i < p.NP; i += kThreads) {
+    uint64_t key = kClosed;
+    if (i < p.N && p.mask[base + i] != 0) {
+      uint32_t hi = 0;
+      if (p.rule == 0) {
+        hi = conf_desc_key(p.conf[base + i]);
+      } else if (p.rule == 2) {
+        hi = uniform_bits(p, b, i);
+      }
+      key = ((uint64_t)hi << 32) | (uint32_t)i;
+      ++mine;
+    }
+    keys[i] = key;
+  }
+  atomicAdd(&n_open, mine);  // integer sum: order-free
+  __syncthreads();
+  // ascending bitonic sort of NP keys (NP a power of two)
+  for (int size = 2; size <= p.NP; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int t = tid; t < p.NP / 2; t += kThreads) {
+        const int lo = 2 * t - (t & (stride - 1));  // first element of the pair
+        const int hi = lo + stride;
+        const bool up = (lo & size) == 0;
+        const uint64_t a = keys[lo], c = keys[hi];
+        if ((a > c) == up) {
+          keys[lo] = c;
+          keys[hi] = a;
+        }
+      }
+      __syncthreads();
+    }
+  }
+  const int n = min(max(p.k[b], 0), n_open);
+  for (int j = tid; j < p.N; j += kThreads) {
+    const int pos = j < n ? (int)(uint32_t)keys[j] : -1;
+    p.order[base + j] = pos;
+    if (j < n) {
+      p.mask[base + pos] = 0;
+      if (p.tokens) p.tokens[base + pos] = p.sample_id[base + pos];
+    }
+  }
+  if (tid == 0 && p.n_revealed) p.n_revealed[b] = n;
+}
+
+hipError_t launch_mdm_reveal(const RevealParams& p, hipStream_t stream) {
+  mdm_reveal_kernel<<<dim3(p.B), dim3(kThreads), 0, stream>>>(p);
+  return hipGetLastError();
+}
+
+int64_t mask_budget_plan(int32_t n_masked, int32_t n_steps, double alpha0, uint64_t seed, int32_t* counts,
+                         int32_t* n_diff_steps) {
+  const int64_t N = n_masked;
+  if (N == 0) {
+    *n_diff_steps = 0;
+    return 0;
+  }
+  int64_t T = n_steps, n_diff = N;
+  if (T == 0) {
+    T = (N + 3) / 4;
+  } else {
+    // Binomial(N, alpha0) as the count of N Bernoulli draws u_i < alpha0;
+    // u_i = uniform of row 0, id i, offset 0: ((x >> 9) + 1/2) * 2^-23, exact
+    // in double
+    n_diff = 0;
+    const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+    for (int64_t q = 0; q * 4 < N; ++q) {
+      const uint4 r = philox4x32_10((uint32_t)q, 0u, 0u, 0u, k0, k1);
+      const uint32_t w[4] = {r.x, r.y, r.z, r.w};
+      for (int j = 0; j < 4 && q * 4 + j < N; ++j) {
+        const double u = ((double)(w[j] >> 9) + 0.5) * 0x1p-23;
+        n_diff += u < alpha0 ? 1 : 0;
+      }
+    }
+  }
+  const int64_t len = T + (N - n_diff);
+  if (counts) {
+    const int64_t base = n_diff / T, extra = n_diff % T;
+    for (int64_t t = 0; t < T; ++t) counts[t] = (int32_t)(base + (t < extra ? 1 : 0));
+    for (int64_t t = T; t < len; ++t) counts[t] = 1;
+  }
+  *n_diff_steps = (int32_t)T;
+  return len;
+}
+
+}  // namespace zarya

@@ -35,7 +35,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_version_and_status_strings():
     L = _lib.lib()
-    assert L.zarya_version() == 3
+    assert L.zarya_version() == 4
     for code, name in [(0, "ZARYA_OK"), (1, "ZARYA_ERR_INVALID_ARGUMENT"), (2, "ZARYA_ERR_UNSUPPORTED"),
                        (3, "ZARYA_ERR_WORKSPACE_TOO_SMALL"), (4, "ZARYA_ERR_HIP")]:
         assert L.zarya_status_string(code).decode() == name

@@ -12,6 +12,10 @@ dim 128, vocab 151936 and the slot shapes are workload choices):
   qwen1.7b  bf16  B=32 Hq/Hkv=16/8  D=128 P=4096  S=16 L=4   H=2048 V=151936
   qwen4b    bf16  B=8  Hq/Hkv=32/8  D=128 P=16384 S=8  L=16  H=2560 V=151936
   layout    bf16  B=8  Hq/Hkv=16/8  D=128 P=0     S=128 L=32 (training layout)
+  modeA     bf16  B=16 Hq/Hkv=16/8  D=128 P=2048  S=260 L=1  H=1024 V=151936
+            (a Mode A denoising step: the 4 tokens revealed at the previous
+            step and the 256 still masked, one causal run after the prompt;
+            the LM head runs on the 256 masked rows of each batch row)
 
 Distributions: Q, K, V ~ N(0, 1); hidden ~ N(0, 1); W ~ N(0, 0.02^2).  Values
 are drawn in float32 and, for bf16 workloads, rounded to bfloat16 with
@@ -73,8 +77,10 @@ WORKLOADS = {
     "qwen1.7b": Workload("qwen1.7b", "bf16", 32, 16, 8, 128, 4096, 16, 4, 2048, 151936, seed=1002),
     "qwen4b": Workload("qwen4b", "bf16", 8, 32, 8, 128, 16384, 8, 16, 2560, 151936, seed=1003),
     "layout": Workload("layout", "bf16", 8, 16, 8, 128, 0, 128, 32, 0, 0, seed=1004),
+    "modeA": Workload("modeA", "bf16", 16, 16, 8, 128, 2048, 260, 1, 1024, 151936, seed=1005),
 }
-WORKLOAD_ORDER = ["tiny", "qwen0.6b", "qwen1.7b", "qwen4b", "layout"]
+WORKLOAD_ORDER = ["tiny", "qwen0.6b", "qwen1.7b", "qwen4b", "layout", "modeA"]
+MODE_A_REVEALED = 4  # rows of the modeA step revealed at the previous step
 
 
 def bf16_bits(x):
