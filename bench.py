@@ -263,6 +263,9 @@ def main():
         result["verification_step"] = verification_step(dev, wl, sets[0], conf_out, sel_out, max(10, args.steps // 2))
         log("timing the sampled LM-head reduction (Gumbel-max, T = 1)")
         result["sampled_draft"] = sampled_draft(dev, wl, sets, max(10, args.steps // 2), conf_ms)
+        if wl.hidden == W.WORKLOADS["modeA"].hidden:
+            log("timing a Mode A denoising step")
+            result["mode_a_step"] = mode_a_step(dev, sets[0]["w_vocab"], max(10, args.steps // 4))
         del sets
         torch.cuda.empty_cache()
         result["layout_attention"] = layout_attention(dev, max(5, args.steps // 10))
@@ -368,6 +371,87 @@ def sampled_draft(dev, wl, sets, K, greedy_ms):
     us = statistics.mean(a.elapsed_time(b) for a, b in evs) * 1e3
     return {"slot_sample_us": us, "tflops": 2.0 * M * V * H / (us * 1e-6) / 1e12,
             "uniforms_per_s": M * V / (us * 1e-6), "vs_greedy_reduction": us / (greedy_ms * 1e3)}
+
+
+def mode_a_step(dev, w_vocab, K):
+    """One denoising step of Mode A (Sec. 5.1) at the modeA workload: causal
+    attention of the 4 tokens revealed at the previous step and the 256 masked
+    ones after a 2048-token prompt, Gumbel-max sampling of the masked rows,
+    the reveal of the 4 most confident, and the cache append of the previous
+    step's 4.  The prefix lengths are reset between steps, outside the timed
+    events."""
+    import numpy as np
+    import torch
+
+    import paper_2609_19868_amd as Z
+    import workloads as W
+
+    wl = W.WORKLOADS["modeA"]
+    B, Hq, Hkv, D, P, R = wl.batch, wl.n_q_heads, wl.n_kv_heads, wl.head_dim, wl.prefix_len, wl.T
+    k_prev = W.MODE_A_REVEALED
+    Nt = R - k_prev
+    x = W.attention_inputs(wl)
+
+    def dev_bf16(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    xd = {k: dev_bf16(v) for k, v in x.items()}
+    kc = torch.empty((B, Hkv, P + k_prev, D), dtype=torch.bfloat16, device=dev)
+    vc = torch.empty_like(kc)
+    kc[:, :, :P].copy_(xd["k_cache"])
+    vc[:, :, :P].copy_(xd["v_cache"])
+    del xd["k_cache"], xd["v_cache"]
+    rng = np.random.default_rng(wl.seed + 7_000_000)
+    hidden = dev_bf16(W.bf16_bits(rng.standard_normal((B * Nt, wl.hidden), dtype=np.float32)))
+    plens0 = torch.full((B,), P, dtype=torch.int32, device=dev)
+    plens = plens0.clone()
+    out = torch.empty((B, Hq, R, D), dtype=torch.bfloat16, device=dev)
+    lse = torch.empty((B, Hq, R), dtype=torch.float32, device=dev)
+    samp = {k: torch.empty(B * Nt, dtype=torch.float32, device=dev) for k in ("sample_prob", "max_prob", "lse")}
+    samp["sample_id"] = torch.empty(B * Nt, dtype=torch.int32, device=dev)
+    mask0 = torch.ones((B, Nt), dtype=torch.uint8, device=dev)
+    mask = mask0.clone()
+    kk = torch.full((B,), k_prev, dtype=torch.int32, device=dev)
+    rev = (torch.empty((B, Nt), dtype=torch.int32, device=dev), torch.empty((B,), dtype=torch.int32, device=dev))
+    acc = torch.zeros((B, R, 1), dtype=torch.uint8, device=dev)
+    acc[:, :k_prev] = 1
+    order = torch.arange(R, dtype=torch.int32, device=dev).repeat(B, 1).contiguous()
+
+    def one(step, evs=None):
+        if evs:
+            evs[0].record()
+        Z.slot_attn(xd["q"], kc, vc, xd["k_slot"], xd["v_slot"], R, 1, pass_=Z.PASS_AR_INFILL,
+                    cross_slot=Z.CROSS_SLOT_CAUSAL, prefix_len=P, out=out, lse=lse, prefix_lens=plens)
+        if evs:
+            evs[1].record()
+        Z.slot_sample(hidden, w_vocab, 1.0, 2025, step, out=samp)
+        if evs:
+            evs[2].record()
+        Z.mdm_reveal(mask, kk, Z.REVEAL_CONFIDENCE, conf=samp["sample_prob"].view(B, Nt), out=rev)
+        if evs:
+            evs[3].record()
+        Z.kv_append(kc, vc, plens, xd["k_slot"], xd["v_slot"], acc, order)
+        if evs:
+            evs[4].record()
+
+    for i in range(3):
+        plens.copy_(plens0)
+        mask.copy_(mask0)
+        one(i)
+    torch.cuda.synchronize()
+    per = []
+    for i in range(K):
+        plens.copy_(plens0)
+        mask.copy_(mask0)
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+        one(100 + i, evs)
+        torch.cuda.synchronize()
+        per.append([evs[j].elapsed_time(evs[j + 1]) * 1e3 for j in range(4)])
+    m = [statistics.mean(p[j] for p in per) for j in range(4)]
+    return {"workload": f"modeA: B={B} Hq/Hkv={Hq}/{Hkv} D={D} P={P} rows={R} ({k_prev} revealed + {Nt} masked) "
+                        f"H={wl.hidden} V={wl.vocab}",
+            "slot_attn_causal_us": m[0], "slot_sample_us": m[1], "mdm_reveal_us": m[2], "kv_append_us": m[3],
+            "step_us": sum(m), "revealed_tokens_per_s": B * k_prev * 1e6 / sum(m)}
 
 
 def copy_calibration(dev, K):
