@@ -39,6 +39,14 @@ METRIC = "slot-scoring steps/s, draft tokens/s; slot_attn HBM GB/s & conf MFMA %
 COUNTERS = os.path.join(ROOT, "profiles", "hbm_traffic_counters.md")
 
 
+def quantile(sorted_vals, q):
+    """Linear-interpolation quantile of an already sorted list."""
+    x = q * (len(sorted_vals) - 1)
+    i = int(x)
+    j = min(i + 1, len(sorted_vals) - 1)
+    return sorted_vals[i] + (sorted_vals[j] - sorted_vals[i]) * (x - i)
+
+
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
@@ -87,7 +95,9 @@ def cpu_baseline(wl, x, c):
                             oracle.CONF_FIRST_TOKEN, oracle.SELECT_THRESHOLD, 0.9, 1)
         times.append(time.perf_counter() - t0)
         log(f"cpu oracle step {rep}: {times[-1]:.2f} s")
-    threads = max([d.get("num_threads", 1) for d in threadpool_info()] + [1])
+    pools = threadpool_info()
+    threads = max([d.get("num_threads", 1) for d in pools] + [1])
+    blas = ",".join(sorted({d.get("internal_api", "?") for d in pools if d.get("user_api") == "blas"})) or "none"
     t = statistics.median(times)
     return {
         "value": 1.0 / t,
@@ -96,7 +106,7 @@ def cpu_baseline(wl, x, c):
         "kind": "oracle",
         "sample": "the whole step (attention of all 16x16 heads x 64 tokens, confidence of all 1024 rows over "
                   "151936 ids, selection), float64 numpy, median of 3 runs; "
-                  f"host has {len(os.sched_getaffinity(0))} usable cores, BLAS threads {threads}",
+                  f"host has {len(os.sched_getaffinity(0))} usable cores, BLAS {blas} with {threads} threads",
         "seconds_per_step": t,
     }
 
@@ -193,10 +203,11 @@ def main():
         total_ms = t_start.elapsed_time(t_end)
         per = [[e[j].elapsed_time(e[j + 1]) for j in range(3)] for e in evs]
         return total_ms / K, [statistics.mean(p[j] for p in per) for j in range(3)], \
-            [statistics.median(p[j] for p in per) for j in range(3)]
+            [statistics.median(p[j] for p in per) for j in range(3)], \
+            [[quantile(sorted(p[j] for p in per), q) for q in (0.1, 0.9)] for j in range(3)]
 
     log(f"timing {args.steps} steps after {args.warmup} warm-up steps (DIFFUSION pass)")
-    ms_step, mean_ms, med_ms = timed(Z.PASS_DIFFUSION, args.steps, args.warmup)
+    ms_step, mean_ms, med_ms, pct_ms = timed(Z.PASS_DIFFUSION, args.steps, args.warmup)
     attn_ms, conf_ms, sel_ms = mean_ms
     log(f"step {ms_step * 1e3:.1f} us: slot_attn {attn_ms * 1e3:.1f} us, slot_confidence {conf_ms * 1e3:.1f} us, "
         f"select_slots {sel_ms * 1e3:.1f} us")
@@ -234,6 +245,8 @@ def main():
         "kernel_us": {"slot_attn": attn_ms * 1e3, "slot_confidence": conf_ms * 1e3, "select_slots": sel_ms * 1e3},
         "kernel_us_median": {"slot_attn": med_ms[0] * 1e3, "slot_confidence": med_ms[1] * 1e3,
                              "select_slots": med_ms[2] * 1e3},
+        "kernel_us_p10_p90": {name: [pct_ms[j][0] * 1e3, pct_ms[j][1] * 1e3]
+                              for j, name in enumerate(("slot_attn", "slot_confidence", "select_slots"))},
         "roofline": {
             "bound": "mfma",
             "kernel": "slot_confidence (GEMM + fused reduction, plus its partial-merge kernel)",
@@ -257,7 +270,7 @@ def main():
 
     if not args.no_extras:
         log("timing the AR_INFILL (verification) pass")
-        ms_ar, mean_ar, _ = timed(Z.PASS_AR_INFILL, max(10, args.steps // 2), 3)
+        ms_ar, mean_ar, _, _ = timed(Z.PASS_AR_INFILL, max(10, args.steps // 2), 3)
         result["ar_infill_pass"] = {"steps_per_s": 1e3 / ms_ar, "slot_attn_us": mean_ar[0] * 1e3}
         log("timing the verification step")
         result["verification_step"] = verification_step(dev, wl, sets[0], conf_out, sel_out, max(10, args.steps // 2))
