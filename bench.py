@@ -430,41 +430,65 @@ def mode_a_step(dev, w_vocab, K):
     acc[:, :k_prev] = 1
     order = torch.arange(R, dtype=torch.int32, device=dev).repeat(B, 1).contiguous()
 
-    def one(step, evs=None):
+    # the first-hitting sampler's order: reveal uniformly random positions,
+    # then sample only those rows (their hidden-row indices, b * Nt + position)
+    samp_sel = {k: torch.empty(B * k_prev, dtype=torch.float32, device=dev)
+                for k in ("sample_prob", "max_prob", "lse")}
+    samp_sel["sample_id"] = torch.empty(B * k_prev, dtype=torch.int32, device=dev)
+    row_base = (torch.arange(B, dtype=torch.int32, device=dev) * Nt).view(B, 1)
+    sel_rows = torch.empty(B * k_prev, dtype=torch.int32, device=dev)
+
+    def one(step, rule, evs=None):
         if evs:
             evs[0].record()
         Z.slot_attn(xd["q"], kc, vc, xd["k_slot"], xd["v_slot"], R, 1, pass_=Z.PASS_AR_INFILL,
                     cross_slot=Z.CROSS_SLOT_CAUSAL, prefix_len=P, out=out, lse=lse, prefix_lens=plens)
         if evs:
             evs[1].record()
-        Z.slot_sample(hidden, w_vocab, 1.0, 2025, step, out=samp)
-        if evs:
-            evs[2].record()
-        Z.mdm_reveal(mask, kk, Z.REVEAL_CONFIDENCE, conf=samp["sample_prob"].view(B, Nt), out=rev)
-        if evs:
-            evs[3].record()
+        if rule == Z.REVEAL_CONFIDENCE:
+            Z.slot_sample(hidden, w_vocab, 1.0, 2025, step, out=samp)
+            if evs:
+                evs[2].record()
+            Z.mdm_reveal(mask, kk, rule, conf=samp["sample_prob"].view(B, Nt), out=rev)
+            if evs:
+                evs[3].record()
+        else:
+            Z.mdm_reveal(mask, kk, rule, seed=2026, offset=step, out=rev)
+            if evs:
+                evs[2].record()
+            # row indices of the revealed positions (index arithmetic on 64 ints, outside the sampled rows' work)
+            torch.add(rev[0][:, :k_prev], row_base, out=sel_rows.view(B, k_prev))
+            Z.slot_sample(hidden, w_vocab, 1.0, 2025, step, rows=sel_rows, out=samp_sel)
+            if evs:
+                evs[3].record()
         Z.kv_append(kc, vc, plens, xd["k_slot"], xd["v_slot"], acc, order)
         if evs:
             evs[4].record()
 
-    for i in range(3):
-        plens.copy_(plens0)
-        mask.copy_(mask0)
-        one(i)
-    torch.cuda.synchronize()
-    per = []
-    for i in range(K):
-        plens.copy_(plens0)
-        mask.copy_(mask0)
-        evs = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
-        one(100 + i, evs)
+    result = {"workload": f"modeA: B={B} Hq/Hkv={Hq}/{Hkv} D={D} P={P} rows={R} ({k_prev} revealed + {Nt} masked) "
+                          f"H={wl.hidden} V={wl.vocab}"}
+    for rule, name in ((Z.REVEAL_CONFIDENCE, "confidence"), (Z.REVEAL_RANDOM, "random")):
+        for i in range(3):
+            plens.copy_(plens0)
+            mask.copy_(mask0)
+            one(i, rule)
         torch.cuda.synchronize()
-        per.append([evs[j].elapsed_time(evs[j + 1]) * 1e3 for j in range(4)])
-    m = [statistics.mean(p[j] for p in per) for j in range(4)]
-    return {"workload": f"modeA: B={B} Hq/Hkv={Hq}/{Hkv} D={D} P={P} rows={R} ({k_prev} revealed + {Nt} masked) "
-                        f"H={wl.hidden} V={wl.vocab}",
-            "slot_attn_causal_us": m[0], "slot_sample_us": m[1], "mdm_reveal_us": m[2], "kv_append_us": m[3],
-            "step_us": sum(m), "revealed_tokens_per_s": B * k_prev * 1e6 / sum(m)}
+        per = []
+        for i in range(K):
+            plens.copy_(plens0)
+            mask.copy_(mask0)
+            evs = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+            one(100 + i, rule, evs)
+            torch.cuda.synchronize()
+            per.append([evs[j].elapsed_time(evs[j + 1]) * 1e3 for j in range(4)])
+        m = [statistics.mean(p[j] for p in per) for j in range(4)]
+        if rule == Z.REVEAL_CONFIDENCE:
+            parts = {"slot_attn_causal_us": m[0], "slot_sample_all_masked_us": m[1], "mdm_reveal_us": m[2]}
+        else:
+            parts = {"slot_attn_causal_us": m[0], "mdm_reveal_us": m[1], "slot_sample_revealed_us": m[2]}
+        result[name] = {**parts, "kv_append_us": m[3], "step_us": sum(m),
+                        "revealed_tokens_per_s": B * k_prev * 1e6 / sum(m)}
+    return result
 
 
 def copy_calibration(dev, K):

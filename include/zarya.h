@@ -67,7 +67,7 @@ extern "C" {
 #endif
 
 #define ZARYA_VERSION_MAJOR 0
-#define ZARYA_VERSION_MINOR 4
+#define ZARYA_VERSION_MINOR 5
 
 typedef enum zarya_status {
   ZARYA_OK = 0,
@@ -322,17 +322,25 @@ typedef struct zarya_sample_params {
 zarya_status zarya_slot_sample_workspace_size(const zarya_conf_desc* desc, size_t* bytes);
 
 /*
- * hidden, w_vocab  as in zarya_slot_confidence
+ * hidden      [M, H] dtype, or [hidden_rows, H] with row_index
+ * row_index   [M] int32 or NULL: output row i samples hidden row row_index[i]
+ *             (the first-hitting sampler draws only the positions it reveals);
+ *             an index outside [0, hidden_rows) gives sample_id -1 and NaN
+ *             probabilities for that row (checked on the GPU).  The random
+ *             stream's row is the output row i in both cases.
+ * hidden_rows rows of hidden when row_index is given (ignored otherwise)
+ * w_vocab     [V, H] dtype
  * sample_id   [M] int32       required
  * sample_prob [M] float32     required
  * max_prob    [M] float32 or NULL
  * lse         [M] float32 or NULL
  * workspace   at least zarya_slot_sample_workspace_size bytes
- * Requires 1/T <= 1e30 (T not denormal-small).
+ * M = desc->n_rows.  Requires 1/T <= 1e30 (T not denormal-small).
  */
 zarya_status zarya_slot_sample(const zarya_conf_desc* desc, const zarya_sample_params* params, const void* hidden,
-                               const void* w_vocab, int32_t* sample_id, float* sample_prob, float* max_prob,
-                               float* lse, void* workspace, size_t workspace_bytes, hipStream_t stream);
+                               const int32_t* row_index, int32_t hidden_rows, const void* w_vocab,
+                               int32_t* sample_id, float* sample_prob, float* max_prob, float* lse, void* workspace,
+                               size_t workspace_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
 /* 7. Mode A: mask budget (host)                                             */

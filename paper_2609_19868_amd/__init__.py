@@ -182,19 +182,25 @@ def slot_confidence(hidden, w_vocab, target_ids=None, out=None, workspace=None):
     return out
 
 
-def slot_sample(hidden, w_vocab, temperature, seed, offset=0, out=None, workspace=None):
+def slot_sample(hidden, w_vocab, temperature, seed, offset=0, rows=None, out=None, workspace=None):
     """Gumbel-max sample of every row of hidden . w_vocab^T at temperature T.
 
-    hidden [M,H], w_vocab [V,H] (bf16 or float32); seed and offset are the
+    hidden [N,H], w_vocab [V,H] (bf16 or float32); seed and offset are the
     64-bit Philox key and counter words (advance offset between draft steps).
+    rows: optional int32 [M] hidden-row indices (output row i samples hidden
+    row rows[i]); without it M = N.
     Returns a dict with ``sample_id`` int32 [M], ``sample_prob`` (the sampled
     token's probability at T = 1), ``max_prob`` and ``lse`` (float32 [M]).
     """
-    M, H = hidden.shape
+    N, H = hidden.shape
     V = w_vocab.shape[0]
     dev, dt = hidden.device, hidden.dtype
-    _need(hidden, "hidden", (M, H), dt, dev)
+    _need(hidden, "hidden", (N, H), dt, dev)
     _need(w_vocab, "w_vocab", (V, H), dt, dev)
+    M = N
+    if rows is not None:
+        M = rows.shape[0]
+        _need(rows, "rows", (M,), torch.int32, dev)
     desc = _lib.ConfDesc(n_rows=M, hidden=H, vocab=V, dtype=_DT[dt])
     params = _lib.SampleParams(temperature=float(temperature), seed=int(seed) & (2**64 - 1),
                                offset=int(offset) & (2**64 - 1))
@@ -205,7 +211,7 @@ def slot_sample(hidden, w_vocab, temperature, seed, offset=0, out=None, workspac
     if workspace is None:
         workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     _lib.check(_lib.lib().zarya_slot_sample(
-        ctypes.byref(desc), ctypes.byref(params), _ptr(hidden), _ptr(w_vocab), _ptr(out["sample_id"]),
+        ctypes.byref(desc), ctypes.byref(params), _ptr(hidden), _ptr(rows), N, _ptr(w_vocab), _ptr(out["sample_id"]),
         _ptr(out["sample_prob"]), _ptr(out.get("max_prob")), _ptr(out.get("lse")), _ptr(workspace),
         workspace.numel(), _stream()))
     return out

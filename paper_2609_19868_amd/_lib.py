@@ -138,8 +138,8 @@ def lib():
         L.zarya_kv_append.restype = ctypes.c_int
         L.zarya_slot_sample_workspace_size.argtypes = [ctypes.POINTER(ConfDesc), ctypes.POINTER(sz)]
         L.zarya_slot_sample_workspace_size.restype = ctypes.c_int
-        L.zarya_slot_sample.argtypes = [ctypes.POINTER(ConfDesc), ctypes.POINTER(SampleParams), vp, vp, vp, vp, vp,
-                                        vp, vp, sz, vp]
+        L.zarya_slot_sample.argtypes = [ctypes.POINTER(ConfDesc), ctypes.POINTER(SampleParams), vp, vp, i32, vp, vp,
+                                        vp, vp, vp, vp, sz, vp]
         L.zarya_slot_sample.restype = ctypes.c_int
         u64, ip = ctypes.c_uint64, ctypes.POINTER(i32)
         L.zarya_mdm_budget.argtypes = [i32, i32, ctypes.c_double, u64, ip, i32, ip, ip]

@@ -140,7 +140,8 @@ zarya_status check_conf_desc(const zarya_conf_desc* d) {
 ConfPlan plan_conf(const zarya_conf_desc* d) {
   ConfPlan pl{};
   if (d->dtype == ZARYA_DTYPE_BF16) {
-    pl.n_rt = (d->n_rows + conf_tile_rows() - 1) / conf_tile_rows();
+    const int br = conf_tile_rows(d->n_rows);
+    pl.n_rt = (d->n_rows + br - 1) / br;
     const int nblk = (d->vocab + 31) / 32;
     // split the vocabulary so that row tiles x vocabulary groups reaches the
     // workgroup count the kernel is tuned for
@@ -162,9 +163,9 @@ size_t sample_ws_bytes(const zarya_conf_desc* d) {
 // Enqueues the LM-head reduction and its merge; with `sp` also the sampling.
 // Arguments are already validated.
 zarya_status run_conf(const zarya_conf_desc* d, const zarya_sample_params* sp, const void* hidden,
-                      const void* w_vocab, const int32_t* target_ids, float* max_prob, int32_t* argmax_id, float* lse,
-                      float* target_prob, int32_t* sample_id, float* sample_prob, void* workspace,
-                      hipStream_t stream) {
+                      const int32_t* row_index, int32_t hidden_rows, const void* w_vocab, const int32_t* target_ids,
+                      float* max_prob, int32_t* argmax_id, float* lse, float* target_prob, int32_t* sample_id,
+                      float* sample_prob, void* workspace, hipStream_t stream) {
   const ConfPlan pl = plan_conf(d);
   (void)hipGetLastError();
   const size_t part = align256((size_t)pl.n_vg * d->n_rows * 4);
@@ -182,6 +183,8 @@ zarya_status run_conf(const zarya_conf_desc* d, const zarya_sample_params* sp, c
   p.part_m = reinterpret_cast<float*>(ws);
   p.part_s = reinterpret_cast<float*>(ws + part);
   p.part_idx = reinterpret_cast<int*>(ws + 2 * part);
+  p.row_index = row_index;
+  p.hidden_rows = hidden_rows;
   if (sp) {
     p.part_g = reinterpret_cast<float*>(ws + 3 * part);
     p.part_gi = reinterpret_cast<int*>(ws + 4 * part);
@@ -214,6 +217,8 @@ zarya_status run_conf(const zarya_conf_desc* d, const zarya_sample_params* sp, c
   mp.part_gi = p.part_gi;
   mp.sample_id = sample_id;
   mp.sample_prob = sample_prob;
+  mp.row_index = row_index;
+  mp.hidden_rows = hidden_rows;
   return hip_status(launch_slot_conf_merge(mp, stream), "LM-head merge launch");
 }
 
@@ -347,8 +352,8 @@ zarya_status zarya_slot_confidence(const zarya_conf_desc* d, const void* hidden,
     return fail(ZARYA_ERR_WORKSPACE_TOO_SMALL, "workspace of %zu bytes is below the %zu required", workspace_bytes,
                 pl.ws_bytes);
   if (!workspace) return fail(ZARYA_ERR_INVALID_ARGUMENT, "workspace is NULL");
-  return run_conf(d, nullptr, hidden, w_vocab, target_ids, max_prob, argmax_id, lse, target_prob, nullptr, nullptr,
-                  workspace, stream);
+  return run_conf(d, nullptr, hidden, nullptr, d->n_rows, w_vocab, target_ids, max_prob, argmax_id, lse, target_prob,
+                  nullptr, nullptr, workspace, stream);
 }
 
 zarya_status zarya_slot_sample_workspace_size(const zarya_conf_desc* desc, size_t* bytes) {
@@ -360,8 +365,9 @@ zarya_status zarya_slot_sample_workspace_size(const zarya_conf_desc* desc, size_
 }
 
 zarya_status zarya_slot_sample(const zarya_conf_desc* d, const zarya_sample_params* sp, const void* hidden,
-                               const void* w_vocab, int32_t* sample_id, float* sample_prob, float* max_prob,
-                               float* lse, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+                               const int32_t* row_index, int32_t hidden_rows, const void* w_vocab, int32_t* sample_id,
+                               float* sample_prob, float* max_prob, float* lse, void* workspace,
+                               size_t workspace_bytes, hipStream_t stream) {
   zarya_status st = check_conf_desc(d);
   if (st != ZARYA_OK) return st;
   if (!sp) return fail(ZARYA_ERR_INVALID_ARGUMENT, "params is NULL");
@@ -370,13 +376,21 @@ zarya_status zarya_slot_sample(const zarya_conf_desc* d, const zarya_sample_para
     return fail(ZARYA_ERR_INVALID_ARGUMENT, "temperature %g must be finite, > 0 and >= 1e-30", (double)T);
   if (!hidden || !w_vocab || !sample_id || !sample_prob)
     return fail(ZARYA_ERR_INVALID_ARGUMENT, "hidden, w_vocab, sample_id and sample_prob are required");
+  if (row_index) {
+    if (hidden_rows < 1) return fail(ZARYA_ERR_INVALID_ARGUMENT, "hidden_rows must be >= 1 with a row_index");
+    if ((int64_t)hidden_rows * d->hidden * 2 >= ((int64_t)1 << 32))
+      return fail(ZARYA_ERR_UNSUPPORTED, "hidden states of %lld bytes exceed 4 GiB",
+                  (long long)hidden_rows * d->hidden * 2);
+  } else {
+    hidden_rows = d->n_rows;
+  }
   const size_t need = sample_ws_bytes(d);
   if (workspace_bytes < need)
     return fail(ZARYA_ERR_WORKSPACE_TOO_SMALL, "workspace of %zu bytes is below the %zu required", workspace_bytes,
                 need);
   if (!workspace) return fail(ZARYA_ERR_INVALID_ARGUMENT, "workspace is NULL");
-  return run_conf(d, sp, hidden, w_vocab, nullptr, max_prob, nullptr, lse, nullptr, sample_id, sample_prob, workspace,
-                  stream);
+  return run_conf(d, sp, hidden, row_index, hidden_rows, w_vocab, nullptr, max_prob, nullptr, lse, nullptr, sample_id,
+                  sample_prob, workspace, stream);
 }
 
 zarya_status zarya_mdm_budget(int32_t n_masked, int32_t n_steps, double alpha0, uint64_t seed, int32_t* counts,

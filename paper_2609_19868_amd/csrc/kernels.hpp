@@ -63,7 +63,17 @@ struct ConfParams {
   int* part_gi;
   float c2t;  // log2(e) / temperature
   uint32_t seed_lo, seed_hi, off_lo, off_hi;
+  // Row selection (null: row i of the output is hidden row i): output row i
+  // is hidden row row_index[i] of hidden_rows (clamped into range here; the
+  // merge marks out-of-range rows).
+  const int32_t* row_index;
+  int hidden_rows;
 };
+
+// Hidden row of output row r.
+__device__ __forceinline__ int conf_hidden_row(const int32_t* row_index, int hidden_rows, int r) {
+  return row_index ? min(max(row_index[r], 0), hidden_rows - 1) : r;
+}
 
 struct ConfMergeParams {
   const float* part_m;
@@ -82,6 +92,8 @@ struct ConfMergeParams {
   const int* part_gi;
   int32_t* sample_id;
   float* sample_prob;
+  const int32_t* row_index;  // as in ConfParams
+  int hidden_rows;
 };
 
 struct SelectParams {
@@ -145,7 +157,7 @@ constexpr int kAttnKeysPerTile = 64;
 constexpr int kAttnRowsPerBlock = 128;
 // hidden rows per workgroup tile and workgroup count the bf16 confidence
 // kernel is tuned for (the vocabulary is split to reach that count)
-int conf_tile_rows();
+int conf_tile_rows(int n_rows);
 int conf_target_workgroups();
 
 hipError_t launch_slot_attn_bf16(const AttnParams& p, int head_dim, hipStream_t stream);

@@ -333,7 +333,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
   for (int j = 0; j < CPB; ++j) {
     const int r = RPC * (NW * j + wave_u) + lrow;
     b_col[j] = 8 * (lcol ^ cswz<BK>(r));
-    b_off[j] = (uint32_t)((size_t)min(row0 + r, p.M - 1) * H + b_col[j]) * 2u;
+    const int xr = conf_hidden_row(p.row_index, p.hidden_rows, min(row0 + r, p.M - 1));
+    b_off[j] = (uint32_t)((size_t)xr * H + b_col[j]) * 2u;
   }
   int cur_vt = -1;
   auto issue_w = [&](int st) {
@@ -495,7 +496,8 @@ __global__ __launch_bounds__(256) void slot_conf_f32_kernel(ConfParams p) {
   const int tid = threadIdx.x;
   const float* X = static_cast<const float*>(p.hidden);
   const float* W = static_cast<const float*>(p.w_vocab);
-  for (int k = tid; k < p.H; k += 256) hs[k] = X[(size_t)row * p.H + k];
+  const size_t xrow = (size_t)conf_hidden_row(p.row_index, p.hidden_rows, row);
+  for (int k = tid; k < p.H; k += 256) hs[k] = X[xrow * p.H + k];
   __syncthreads();
   const int v_lo = (int)((long long)vg * p.V / p.n_vg);
   const int v_hi = (int)((long long)(vg + 1) * p.V / p.n_vg);
@@ -565,14 +567,14 @@ __global__ __launch_bounds__(256) void slot_conf_f32_kernel(ConfParams p) {
 
 // Logit of vocab id v for a row, hidden . w_vocab[v], as a float32 dot
 // product spread over the 64 lanes of a wave (every lane gets the sum).
-__device__ float row_logit(const ConfMergeParams& p, int row, int v, int lane) {
+__device__ float row_logit(const ConfMergeParams& p, int hrow, int v, int lane) {
   float z = 0.f;
   if (p.bf16) {
-    const uint16_t* hr = static_cast<const uint16_t*>(p.hidden) + (size_t)row * p.H;
+    const uint16_t* hr = static_cast<const uint16_t*>(p.hidden) + (size_t)hrow * p.H;
     const uint16_t* wr = static_cast<const uint16_t*>(p.w_vocab) + (size_t)v * p.H;
     for (int k = lane; k < p.H; k += 64) z = fmaf(bf16_to_f32(hr[k]), bf16_to_f32(wr[k]), z);
   } else {
-    const float* hr = static_cast<const float*>(p.hidden) + (size_t)row * p.H;
+    const float* hr = static_cast<const float*>(p.hidden) + (size_t)hrow * p.H;
     const float* wr = static_cast<const float*>(p.w_vocab) + (size_t)v * p.H;
     for (int k = lane; k < p.H; k += 64) z = fmaf(hr[k], wr[k], z);
   }
@@ -612,23 +614,30 @@ __global__ __launch_bounds__(256) void slot_conf_merge_kernel(ConfMergeParams p)
   const float lse2 = m * kLog2e + __log2f(s);
   const int tgt = p.target_ids ? p.target_ids[row] : -1;
   const bool tgt_ok = tgt >= 0 && tgt < p.V;
-  const float zt = tgt_ok ? row_logit(p, row, tgt, lane) : 0.f;
+  const int hrow = conf_hidden_row(p.row_index, p.hidden_rows, row);
+  const float zt = tgt_ok ? row_logit(p, hrow, tgt, lane) : 0.f;
   // every row has a finite perturbed score, so sgi is a valid id
-  const float zs = p.part_g ? row_logit(p, row, sgi, lane) : 0.f;
+  const float zs = p.part_g ? row_logit(p, hrow, sgi, lane) : 0.f;
   if (lane != 0) return;
-  if (p.max_prob) p.max_prob[row] = 1.f / s;
-  if (p.argmax_id) p.argmax_id[row] = idx;
-  if (p.lse) p.lse[row] = lse2 * kLn2;
+  // a row index outside the hidden rows was clamped for the loads: mark its results
+  const bool bad = p.row_index && (p.row_index[row] < 0 || p.row_index[row] >= p.hidden_rows);
+  const float nan = __builtin_nanf("");
+  if (p.max_prob) p.max_prob[row] = bad ? nan : 1.f / s;
+  if (p.argmax_id) p.argmax_id[row] = bad ? -1 : idx;
+  if (p.lse) p.lse[row] = bad ? nan : lse2 * kLn2;
   if (p.part_g) {
-    p.sample_id[row] = sgi;
-    p.sample_prob[row] = fast_exp2(zs * kLog2e - lse2);
+    p.sample_id[row] = bad ? -1 : sgi;
+    p.sample_prob[row] = bad ? nan : fast_exp2(zs * kLog2e - lse2);
   }
-  if (p.target_ids && p.target_prob) p.target_prob[row] = tgt_ok ? fast_exp2(zt * kLog2e - lse2) : __builtin_nanf("");
+  if (p.target_ids && p.target_prob) p.target_prob[row] = tgt_ok && !bad ? fast_exp2(zt * kLog2e - lse2) : nan;
 }
 
 // Tile configuration (measured on MI355X over the 0.6B/1.7B/4B LM-head
 // shapes): 8 waves over a 256 x 256 tile, 64-deep stages, three W and two
-// hidden LDS buffers (160 KB), one workgroup per compute unit.
+// hidden LDS buffers (160 KB), one workgroup per compute unit.  With few rows
+// (a single sequence's draft tokens, the tokens a first-hitting step reveals)
+// most of a 256-row tile would be padding and the reduction is bound by the
+// W stream instead: 4 waves over a 256 x 64 tile.
 #ifndef ZARYA_CONF_NW
 #define ZARYA_CONF_NW 8
 #endif
@@ -647,17 +656,30 @@ __global__ __launch_bounds__(256) void slot_conf_merge_kernel(ConfMergeParams p)
 #ifndef ZARYA_CONF_WGS
 #define ZARYA_CONF_WGS 256  // workgroups to aim for: one per compute unit
 #endif
+#ifndef ZARYA_CONF_SMALL_M
+#define ZARYA_CONF_SMALL_M 128  // row counts up to this take the 64-row tile (measured crossover)
+#endif
+constexpr int kSmallNW = 4, kSmallBR = 64;
 
-int conf_tile_rows() { return ZARYA_CONF_BR; }
+int conf_tile_rows(int n_rows) { return n_rows <= ZARYA_CONF_SMALL_M ? kSmallBR : ZARYA_CONF_BR; }
 int conf_target_workgroups() { return ZARYA_CONF_WGS; }
 
 hipError_t launch_slot_conf_bf16(const ConfParams& p, hipStream_t stream) {
-  if (p.part_g) {
+  const dim3 grid(8 * p.per_xcd);
+  if (conf_tile_rows(p.M) == kSmallBR) {
+    if (p.part_g) {
+      slot_conf_bf16_kernel<kSmallNW, kSmallBR, ZARYA_CONF_BK, ZARYA_CONF_NSW, ZARYA_CONF_NSX, true>
+          <<<grid, dim3(kSmallNW * 64), 0, stream>>>(p);
+    } else {
+      slot_conf_bf16_kernel<kSmallNW, kSmallBR, ZARYA_CONF_BK, ZARYA_CONF_NSW, ZARYA_CONF_NSX, false>
+          <<<grid, dim3(kSmallNW * 64), 0, stream>>>(p);
+    }
+  } else if (p.part_g) {
     slot_conf_bf16_kernel<ZARYA_CONF_NW, ZARYA_CONF_BR, ZARYA_CONF_BK, ZARYA_CONF_NSW, ZARYA_CONF_NSX, true>
-        <<<dim3(8 * p.per_xcd), dim3(ZARYA_CONF_NW * 64), 0, stream>>>(p);
+        <<<grid, dim3(ZARYA_CONF_NW * 64), 0, stream>>>(p);
   } else {
     slot_conf_bf16_kernel<ZARYA_CONF_NW, ZARYA_CONF_BR, ZARYA_CONF_BK, ZARYA_CONF_NSW, ZARYA_CONF_NSX, false>
-        <<<dim3(8 * p.per_xcd), dim3(ZARYA_CONF_NW * 64), 0, stream>>>(p);
+        <<<grid, dim3(ZARYA_CONF_NW * 64), 0, stream>>>(p);
   }
   return hipGetLastError();
 }

@@ -35,7 +35,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_version_and_status_strings():
     L = _lib.lib()
-    assert L.zarya_version() == 4
+    assert L.zarya_version() == 5
     for code, name in [(0, "ZARYA_OK"), (1, "ZARYA_ERR_INVALID_ARGUMENT"), (2, "ZARYA_ERR_UNSUPPORTED"),
                        (3, "ZARYA_ERR_WORKSPACE_TOO_SMALL"), (4, "ZARYA_ERR_HIP")]:
         assert L.zarya_status_string(code).decode() == name
@@ -129,14 +129,15 @@ def test_slot_confidence_workspace_checks():
     assert _conf_status(d, ptr=0) == _lib.ERR_INVALID_ARGUMENT
 
 
-def _sample_status(desc, temperature=1.0, ptr=1, ws_bytes=1 << 40, params=True, out_null=None):
+def _sample_status(desc, temperature=1.0, ptr=1, ws_bytes=1 << 40, params=True, out_null=None, rows=None,
+                   hidden_rows=0):
     p = ctypes.c_void_p(ptr) if ptr else None
     sp = _lib.SampleParams(temperature=temperature, seed=1, offset=2)
     outs = [p, p]
     if out_null is not None:
         outs[out_null] = None
-    return _lib.lib().zarya_slot_sample(ctypes.byref(desc), ctypes.byref(sp) if params else None, p, p, *outs,
-                                        None, None, p, ws_bytes, None)
+    return _lib.lib().zarya_slot_sample(ctypes.byref(desc), ctypes.byref(sp) if params else None, p, rows,
+                                        hidden_rows, p, *outs, None, None, p, ws_bytes, None)
 
 
 @pytest.mark.parametrize("temperature", [0.0, -1.0, float("nan"), float("inf"), 1e-31])
@@ -157,6 +158,10 @@ def test_slot_sample_argument_checks():
     assert _sample_status(d, params=False) == _lib.ERR_INVALID_ARGUMENT
     assert _sample_status(d, out_null=0) == _lib.ERR_INVALID_ARGUMENT  # sample_id is required
     assert _sample_status(d, out_null=1) == _lib.ERR_INVALID_ARGUMENT  # sample_prob is required
+    # a row selection needs the hidden row count, and its bytes must stay below 4 GiB
+    r = ctypes.c_void_p(1)
+    assert _sample_status(d, rows=r, hidden_rows=0) == _lib.ERR_INVALID_ARGUMENT
+    assert _sample_status(d, rows=r, hidden_rows=1 << 21) == _lib.ERR_UNSUPPORTED
     for bad, code in [(dict(n_rows=0), _lib.ERR_INVALID_ARGUMENT), (dict(hidden=1001), _lib.ERR_UNSUPPORTED)]:
         base = dict(n_rows=64, hidden=1024, vocab=151936, dtype=1)
         base.update(bad)

@@ -56,6 +56,8 @@ SMALL = [
     ("m40_v2049_h136", dict(batch=1, n_slots=8, slot_len=5, hidden=136, vocab=2049)),
     ("m1_v100_h64", dict(batch=1, n_slots=1, slot_len=1, hidden=64, vocab=100)),
     ("m513_v33000_h1024", dict(batch=1, n_slots=27, slot_len=19, hidden=1024, vocab=33000)),
+    ("m128_v7001_h512", dict(batch=1, n_slots=16, slot_len=8, hidden=512, vocab=7001)),  # largest 64-row-tile case
+    ("m129_v7001_h512", dict(batch=1, n_slots=43, slot_len=3, hidden=512, vocab=7001)),  # smallest 256-row-tile case
 ]
 
 

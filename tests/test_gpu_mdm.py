@@ -86,7 +86,9 @@ def _x_bits(t):
 @pytest.mark.parametrize("rule,rname", RULES[::2], ids=[r[1] for r in RULES[::2]])
 def test_generation_chain(rule, rname):
     """A whole Mode A generation: 2 rows of 30 masks after a 100-token prompt,
-    T = 0 (steps of at most four), every stage against the oracle."""
+    T = 0 (steps of at most four), every stage against the oracle.  The
+    confidence rule samples every masked row, then reveals; the random rule
+    (first-hitting sampler) reveals first and samples only the chosen rows."""
     dev = require_gpu()
     B, Hq, Hkv, D, P0, N0, H, V = 2, 4, 2, 128, 100, 30, 256, 3000
     scale = 1.0 / np.sqrt(D)
@@ -140,34 +142,53 @@ def test_generation_chain(rule, rname):
         if Nt == 0:
             break
 
-        # LM head with Gumbel-max sampling on the masked rows (row i = b * Nt + j)
         hid = W.bf16_bits(rng.standard_normal((B * Nt, H)).astype(np.float32))
-        res = Z.slot_sample(to_dev(hid, "bf16", dev), wd, 1.0, seed=11, offset=t)
-        torch.cuda.synchronize()
-        ref = oracle.slot_sample(W.as_f64(hid, "bf16"), W.as_f64(w, "bf16"), 1.0, 11, t)
-        sid = res["sample_id"].cpu().numpy()
-        decided = ref["score_gap"] >= 1e-3
-        assert np.array_equal(sid[decided], ref["sample_id"][decided]), f"step {t} sampling"
-        sp = res["sample_prob"].view(B, Nt).contiguous()
-
-        # reveal k_t of the masked tail
+        hd = to_dev(hid, "bf16", dev)
         mask = torch.ones((B, Nt), dtype=torch.uint8, device=dev)
         kk = torch.full((B,), k_t, dtype=torch.int32, device=dev)
-        tok_t = torch.full((B, Nt), -1, dtype=torch.int32, device=dev)
-        sid_t = res["sample_id"].view(B, Nt).contiguous()
-        order, n = Z.mdm_reveal(mask, kk, rule, conf=sp, seed=13, offset=t, sample_id=sid_t, tokens=tok_t)
-        torch.cuda.synchronize()
-        o_ref, n_ref, m_ref, t_ref = oracle.reveal(sp.cpu().numpy(), np.ones((B, Nt), bool), [k_t] * B, rule, 13,
-                                                   t, tokens=np.full((B, Nt), -1), sample_id=sid.reshape(B, Nt))
-        assert np.array_equal(order.cpu().numpy(), o_ref) and np.array_equal(n.cpu().numpy(), n_ref)
-        assert np.array_equal(mask.cpu().numpy().astype(bool), m_ref)
-        assert np.array_equal(tok_t.cpu().numpy(), t_ref)
+        if rule == Z.REVEAL_RANDOM:
+            # first-hitting sampler: choose the positions, then draw only their tokens
+            order, n = Z.mdm_reveal(mask, kk, rule, seed=13, offset=t)
+            torch.cuda.synchronize()
+            o_ref, n_ref, m_ref, _ = oracle.reveal(None, np.ones((B, Nt), bool), [k_t] * B, rule, 13, t)
+            assert np.array_equal(order.cpu().numpy(), o_ref) and np.array_equal(n.cpu().numpy(), n_ref)
+            assert np.array_equal(mask.cpu().numpy().astype(bool), m_ref)
+            sel = np.concatenate([b * Nt + o_ref[b, : n_ref[b]] for b in range(B)]).astype(np.int32)
+            res = Z.slot_sample(hd, wd, 1.0, seed=11, offset=t, rows=torch.from_numpy(sel).to(dev))
+            torch.cuda.synchronize()
+            ref = oracle.slot_sample(W.as_f64(hid[sel], "bf16"), W.as_f64(w, "bf16"), 1.0, 11, t)
+            sid_sel = res["sample_id"].cpu().numpy()
+            decided = ref["score_gap"] >= 1e-3
+            assert np.array_equal(sid_sel[decided], ref["sample_id"][decided]), f"step {t} sampling"
+            drawn = np.full((B, Nt), -1, dtype=np.int64)
+            drawn.reshape(-1)[sel] = sid_sel
+        else:
+            # LM head with Gumbel-max sampling on every masked row (row i = b * Nt + j)
+            res = Z.slot_sample(hd, wd, 1.0, seed=11, offset=t)
+            torch.cuda.synchronize()
+            ref = oracle.slot_sample(W.as_f64(hid, "bf16"), W.as_f64(w, "bf16"), 1.0, 11, t)
+            sid = res["sample_id"].cpu().numpy()
+            decided = ref["score_gap"] >= 1e-3
+            assert np.array_equal(sid[decided], ref["sample_id"][decided]), f"step {t} sampling"
+            sp = res["sample_prob"].view(B, Nt).contiguous()
+            # reveal the k_t most confident of the masked tail, writing their tokens
+            tok_t = torch.full((B, Nt), -1, dtype=torch.int32, device=dev)
+            sid_t = res["sample_id"].view(B, Nt).contiguous()
+            order, n = Z.mdm_reveal(mask, kk, rule, conf=sp, seed=13, offset=t, sample_id=sid_t, tokens=tok_t)
+            torch.cuda.synchronize()
+            o_ref, n_ref, m_ref, t_ref = oracle.reveal(sp.cpu().numpy(), np.ones((B, Nt), bool), [k_t] * B, rule,
+                                                       13, t, tokens=np.full((B, Nt), -1),
+                                                       sample_id=sid.reshape(B, Nt))
+            assert np.array_equal(order.cpu().numpy(), o_ref) and np.array_equal(n.cpu().numpy(), n_ref)
+            assert np.array_equal(mask.cpu().numpy().astype(bool), m_ref)
+            assert np.array_equal(tok_t.cpu().numpy(), t_ref)
+            drawn = sid.reshape(B, Nt)
         o = order.cpu().numpy()
         for b in range(B):
             picked = [tail[b][j] for j in o[b, : n_ref[b]]]
             for j, pos in zip(o[b, : n_ref[b]], picked):
-                assert tokens[b, pos] == -1
-                tokens[b, pos] = sid.reshape(B, Nt)[b, j]
+                assert tokens[b, pos] == -1 and drawn[b, j] >= 0
+                tokens[b, pos] = drawn[b, j]
             tail[b] = [tail[b][j] for j in range(Nt) if m_ref[b, j]]
         prev = int(n_ref[0])
     assert np.all(tokens >= 0), "every masked position is revealed exactly once"

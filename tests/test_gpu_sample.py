@@ -31,9 +31,11 @@ def _planted(M, V, n, seed):
     return rows, rng.integers(0, V, size=len(rows)), rng.uniform(0.0, 120.0, size=len(rows))
 
 
-def _check(res, hf, wf, T, seed, offset, rows, f32, what):
-    """Compare the GPU results of `rows` with the oracle on the same rows."""
-    ref = oracle.slot_sample(hf, wf, T, seed, offset, row_ids=rows)
+def _check(res, hf, wf, T, seed, offset, rows, f32, what, row_ids=None):
+    """Compare the GPU results of `rows` with the oracle on the same rows
+    (`row_ids`: the rows' indices in the random stream, default `rows`)."""
+    row_ids = rows if row_ids is None else row_ids
+    ref = oracle.slot_sample(hf, wf, T, seed, offset, row_ids=row_ids)
     conf = oracle.slot_confidence(hf, wf)
     tol = 1e-4 if f32 else 1e-3
     sid = res["sample_id"].cpu().numpy()[rows].astype(np.int64)
@@ -47,7 +49,7 @@ def _check(res, hf, wf, T, seed, offset, rows, f32, what):
     mism = decided & (sid != ref["sample_id"])
     assert not mism.any(), f"{what}: {mism.sum()} of {decided.sum()} decided rows sampled a different id"
     for i in np.flatnonzero(~decided):  # near-ties: the GPU's pick must be a near-winner
-        u = oracle.uniforms([rows[i]], V, seed, offset)[0, sid[i]]
+        u = oracle.uniforms([row_ids[i]], V, seed, offset)[0, sid[i]]
         score = float(hf[i] @ wf[sid[i]]) / T + float(oracle.gumbel(u))
         assert ref["best_score"][i] - score <= gap_tol, f"{what}: row {rows[i]} id {sid[i]} is not a near-winner"
     # probability of the id the GPU drew, from the oracle's logits
@@ -86,6 +88,8 @@ SMALL = [
     ("m40_v2049_h136", dict(batch=1, n_slots=8, slot_len=5, hidden=136, vocab=2049)),
     ("m1_v100_h64", dict(batch=1, n_slots=1, slot_len=1, hidden=64, vocab=100)),
     ("m513_v33000_h1024", dict(batch=1, n_slots=27, slot_len=19, hidden=1024, vocab=33000)),
+    ("m128_v7001_h512", dict(batch=1, n_slots=16, slot_len=8, hidden=512, vocab=7001)),  # largest 64-row-tile case
+    ("m129_v7001_h512", dict(batch=1, n_slots=43, slot_len=3, hidden=512, vocab=7001)),  # smallest 256-row-tile case
 ]
 
 
@@ -162,3 +166,35 @@ def test_full_size_sampled(name):
     rows = np.unique(np.concatenate([rng.choice(wl.M, 40, replace=False), [0, wl.M - 1], plant[0]]))
     say(f"slot_sample full {name}: generating inputs")
     _run(wl, dev, 1.0, rows=rows, plant=plant, what=f"full {name}")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_row_selection(dtype):
+    """Output row i samples hidden row rows[i] (duplicates allowed) with the
+    stream of output row i; indices outside the hidden rows give -1 / NaN."""
+    dev = require_gpu()
+    base = W.WORKLOADS["qwen0.6b"] if dtype == "bf16" else W.WORKLOADS["tiny"]
+    wl = base.replace(batch=1, n_slots=60, slot_len=5, hidden=256 if dtype == "bf16" else 128,
+                      vocab=33000 if dtype == "bf16" else 700, seed=97)
+    c = W.confidence_inputs(wl, plant=_planted(wl.M, wl.vocab, 40, 6))
+    N = wl.M
+    rng = np.random.default_rng(98)
+    rows = rng.integers(0, N, 130).astype(np.int32)
+    rows[[3, 77]] = rows[5]  # duplicates
+    rows[10], rows[100] = -1, N  # out of range
+    hd, wd = to_dev(c["hidden"], dtype, dev), to_dev(c["w_vocab"], dtype, dev)
+    say(f"slot_sample row selection {dtype} N={N} M={rows.size}")
+    res = Z.slot_sample(hd, wd, 0.8, SEED, OFFSET, rows=torch.from_numpy(rows).to(dev))
+    torch.cuda.synchronize()
+    bad = (rows < 0) | (rows >= N)
+    sid = res["sample_id"].cpu().numpy()
+    assert np.all(sid[bad] == -1)
+    for k in ("sample_prob", "max_prob", "lse"):
+        assert np.all(np.isnan(res[k].cpu().numpy()[bad])), k
+    ok = np.flatnonzero(~bad)
+    hf = W.as_f64(c["hidden"][rows[ok]], dtype)
+    wf = W.as_f64(c["w_vocab"], dtype)
+    # the oracle on the selected hidden rows, each with its output row's stream
+    sub = {k: v[torch.from_numpy(ok).to(dev)] for k, v in res.items()}
+    _check(sub, hf, wf, 0.8, SEED, OFFSET, np.arange(ok.size), dtype == "f32", f"row selection {dtype}",
+           row_ids=ok)
