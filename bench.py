@@ -281,6 +281,8 @@ def main():
             result["mode_a_step"] = mode_a_step(dev, sets[0]["w_vocab"], max(10, args.steps // 4))
         del sets
         torch.cuda.empty_cache()
+        log("timing the single-sequence step (batch 1)")
+        result["single_sequence_step"] = single_sequence_step(dev, wl, max(20, args.steps // 2))
         result["layout_attention"] = layout_attention(dev, max(5, args.steps // 10))
 
     if not args.no_cpu_baseline:
@@ -510,6 +512,62 @@ def copy_calibration(dev, K):
     ms = a.elapsed_time(b) / K
     print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "us": ms * 1e3,
                       "gbps": 2 * n / (ms * 1e-3) / 1e9}), flush=True)
+
+
+def single_sequence_step(dev, wl, K):
+    """The scoring step of one sequence (batch 1 of the same model and slot
+    shape): the latency a single request sees.  Its 64 draft rows take the
+    reduction's 64-row tile.  Inputs rotate over three copies of W."""
+    import numpy as np
+    import torch
+
+    import paper_2609_19868_amd as Z
+    import workloads as W
+
+    w1 = wl.replace(batch=1, seed=wl.seed + 11)
+    x = W.attention_inputs(w1)
+    c = W.confidence_inputs(w1)
+
+    def dev_bf16(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    xd = {k: dev_bf16(v) for k, v in x.items()}
+    h = dev_bf16(c["hidden"])
+    ws = [dev_bf16(c["w_vocab"])]
+    ws += [ws[0].clone() for _ in range(2)]
+    S, L = w1.n_slots, w1.slot_len
+
+    def one(i, evs=None):
+        if evs:
+            evs[0].record()
+        Z.slot_attn(xd["q"], xd["k_cache"], xd["v_cache"], xd["k_slot"], xd["v_slot"], S, L,
+                    pass_=Z.PASS_DIFFUSION)
+        if evs:
+            evs[1].record()
+        r = Z.slot_confidence(h, ws[i % 3])
+        if evs:
+            evs[2].record()
+        Z.select_slots(r["max_prob"].view(1, S, L), threshold=0.9)
+        if evs:
+            evs[3].record()
+
+    for i in range(5):
+        one(i)
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for i in range(K):
+        one(i)
+    t1.record()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    for i in range(K):
+        one(i, evs[i])
+    torch.cuda.synchronize()
+    m = [statistics.mean(e[j].elapsed_time(e[j + 1]) * 1e3 for e in evs) for j in range(3)]
+    us = t0.elapsed_time(t1) / K * 1e3
+    return {"workload": f"{wl.name} shapes at batch 1 ({S * L} draft rows)", "step_us": us,
+            "steps_per_s": 1e6 / us, "slot_attn_us": m[0], "slot_confidence_us": m[1], "select_slots_us": m[2]}
 
 
 def layout_attention(dev, K):
