@@ -566,8 +566,34 @@ def single_sequence_step(dev, wl, K):
     torch.cuda.synchronize()
     m = [statistics.mean(e[j].elapsed_time(e[j + 1]) * 1e3 for e in evs) for j in range(3)]
     us = t0.elapsed_time(t1) / K * 1e3
+
+    # The same step captured in HIP graphs (one per W copy) and replayed: the
+    # host-side launch cost of the three calls leaves the critical path.
+    graphs = []
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for i in range(3):
+            one(i)
+    torch.cuda.current_stream().wait_stream(side)
+    for i in range(3):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            one(i)
+        graphs.append(g)
+    torch.cuda.synchronize()
+    for i in range(3):
+        graphs[i].replay()
+    torch.cuda.synchronize()
+    t0.record()
+    for i in range(K):
+        graphs[i % 3].replay()
+    t1.record()
+    torch.cuda.synchronize()
+    us_graph = t0.elapsed_time(t1) / K * 1e3
     return {"workload": f"{wl.name} shapes at batch 1 ({S * L} draft rows)", "step_us": us,
-            "steps_per_s": 1e6 / us, "slot_attn_us": m[0], "slot_confidence_us": m[1], "select_slots_us": m[2]}
+            "steps_per_s": 1e6 / us, "slot_attn_us": m[0], "slot_confidence_us": m[1], "select_slots_us": m[2],
+            "graph_step_us": us_graph, "graph_steps_per_s": 1e6 / us_graph}
 
 
 def layout_attention(dev, K):
