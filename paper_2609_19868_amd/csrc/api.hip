@@ -147,7 +147,7 @@ ConfPlan plan_conf(const zarya_conf_desc* d) {
     const int nblk = (d->vocab + 31) / 32;
     // split the vocabulary so that row tiles x vocabulary groups reaches the
     // workgroup count the kernel is tuned for
-    pl.n_vg = std::max(1, std::min(nblk, conf_target_workgroups() / pl.n_rt));
+    pl.n_vg = std::max(1, std::min(nblk, kConfTargetWGs / pl.n_rt));
   } else {
     pl.n_rt = 1;
     pl.n_vg = std::max(1, std::min(64, d->vocab / 2048));

@@ -155,10 +155,18 @@ constexpr int kAppendMaxTokens = 8192;
 
 constexpr int kAttnKeysPerTile = 64;
 constexpr int kAttnRowsPerBlock = 128;
-// hidden rows per workgroup tile and workgroup count the bf16 confidence
-// kernel is tuned for (the vocabulary is split to reach that count)
-int conf_tile_rows(int n_rows);
-int conf_target_workgroups();
+// Tile configuration of the bf16 LM-head reduction (measured on MI355X over
+// the 0.6B/1.7B/4B shapes): 8 waves over a 256 x 256 tile, 64-deep stages,
+// three W and two hidden LDS buffers (160 KB), one workgroup per compute
+// unit.  With few rows (a single sequence's draft tokens, the tokens a
+// first-hitting step reveals) most of a 256-row tile would be padding and the
+// reduction is bound by the W stream instead: 4 waves over a 256 x 64 tile,
+// up to 128 rows (the measured crossover).  The vocabulary is split into
+// groups until row tiles x groups reaches kConfTargetWGs (one per CU).
+constexpr int kConfNW = 8, kConfBR = 256, kConfBK = 64, kConfNSW = 3, kConfNSX = 2;
+constexpr int kConfSmallNW = 4, kConfSmallBR = 64, kConfSmallMaxRows = 128;
+constexpr int kConfTargetWGs = 256;
+constexpr int conf_tile_rows(int n_rows) { return n_rows <= kConfSmallMaxRows ? kConfSmallBR : kConfBR; }
 
 hipError_t launch_slot_attn_bf16(const AttnParams& p, int head_dim, hipStream_t stream);
 hipError_t launch_slot_attn_f32(const AttnParams32& p, int head_dim, hipStream_t stream);

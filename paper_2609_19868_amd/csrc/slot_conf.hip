@@ -268,7 +268,7 @@ __device__ __forceinline__ void store_partials(const ConfParams& p, int vg, int 
 // (re-read for every vocab tile, so served from L2) through a ring of NSX.
 // Partials are written per (vocabulary group, row).
 template <int NW, int BR, int BK, int NSW, int NSX, bool SAMPLE>
-__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) void slot_conf_bf16_kernel(
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4))) void slot_conf_bf16_kernel(
     ConfParams p) {
   constexpr int ATB = BV * BK * 2;    // bytes of the W tile of one stage
   constexpr int BTB = BR * BK * 2;    // bytes of the hidden tile of one stage
@@ -632,54 +632,22 @@ __global__ __launch_bounds__(256) void slot_conf_merge_kernel(ConfMergeParams p)
   if (p.target_ids && p.target_prob) p.target_prob[row] = tgt_ok && !bad ? fast_exp2(zt * kLog2e - lse2) : nan;
 }
 
-// Tile configuration (measured on MI355X over the 0.6B/1.7B/4B LM-head
-// shapes): 8 waves over a 256 x 256 tile, 64-deep stages, three W and two
-// hidden LDS buffers (160 KB), one workgroup per compute unit.  With few rows
-// (a single sequence's draft tokens, the tokens a first-hitting step reveals)
-// most of a 256-row tile would be padding and the reduction is bound by the
-// W stream instead: 4 waves over a 256 x 64 tile.
-#ifndef ZARYA_CONF_NW
-#define ZARYA_CONF_NW 8
-#endif
-#ifndef ZARYA_CONF_BR
-#define ZARYA_CONF_BR 256
-#endif
-#ifndef ZARYA_CONF_BK
-#define ZARYA_CONF_BK 64
-#endif
-#ifndef ZARYA_CONF_NSW
-#define ZARYA_CONF_NSW 3
-#endif
-#ifndef ZARYA_CONF_NSX
-#define ZARYA_CONF_NSX 2
-#endif
-#ifndef ZARYA_CONF_WGS
-#define ZARYA_CONF_WGS 256  // workgroups to aim for: one per compute unit
-#endif
-#ifndef ZARYA_CONF_SMALL_M
-#define ZARYA_CONF_SMALL_M 128  // row counts up to this take the 64-row tile (measured crossover)
-#endif
-constexpr int kSmallNW = 4, kSmallBR = 64;
-
-int conf_tile_rows(int n_rows) { return n_rows <= ZARYA_CONF_SMALL_M ? kSmallBR : ZARYA_CONF_BR; }
-int conf_target_workgroups() { return ZARYA_CONF_WGS; }
-
 hipError_t launch_slot_conf_bf16(const ConfParams& p, hipStream_t stream) {
   const dim3 grid(8 * p.per_xcd);
-  if (conf_tile_rows(p.M) == kSmallBR) {
+  if (conf_tile_rows(p.M) == kConfSmallBR) {
     if (p.part_g) {
-      slot_conf_bf16_kernel<kSmallNW, kSmallBR, ZARYA_CONF_BK, ZARYA_CONF_NSW, ZARYA_CONF_NSX, true>
-          <<<grid, dim3(kSmallNW * 64), 0, stream>>>(p);
+      slot_conf_bf16_kernel<kConfSmallNW, kConfSmallBR, kConfBK, kConfNSW, kConfNSX, true>
+          <<<grid, dim3(kConfSmallNW * 64), 0, stream>>>(p);
     } else {
-      slot_conf_bf16_kernel<kSmallNW, kSmallBR, ZARYA_CONF_BK, ZARYA_CONF_NSW, ZARYA_CONF_NSX, false>
-          <<<grid, dim3(kSmallNW * 64), 0, stream>>>(p);
+      slot_conf_bf16_kernel<kConfSmallNW, kConfSmallBR, kConfBK, kConfNSW, kConfNSX, false>
+          <<<grid, dim3(kConfSmallNW * 64), 0, stream>>>(p);
     }
   } else if (p.part_g) {
-    slot_conf_bf16_kernel<ZARYA_CONF_NW, ZARYA_CONF_BR, ZARYA_CONF_BK, ZARYA_CONF_NSW, ZARYA_CONF_NSX, true>
-        <<<grid, dim3(ZARYA_CONF_NW * 64), 0, stream>>>(p);
+    slot_conf_bf16_kernel<kConfNW, kConfBR, kConfBK, kConfNSW, kConfNSX, true>
+        <<<grid, dim3(kConfNW * 64), 0, stream>>>(p);
   } else {
-    slot_conf_bf16_kernel<ZARYA_CONF_NW, ZARYA_CONF_BR, ZARYA_CONF_BK, ZARYA_CONF_NSW, ZARYA_CONF_NSX, false>
-        <<<grid, dim3(ZARYA_CONF_NW * 64), 0, stream>>>(p);
+    slot_conf_bf16_kernel<kConfNW, kConfBR, kConfBK, kConfNSW, kConfNSX, false>
+        <<<grid, dim3(kConfNW * 64), 0, stream>>>(p);
   }
   return hipGetLastError();
 }

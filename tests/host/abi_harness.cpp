@@ -1,0 +1,255 @@
+// Host-side checks of libzarya's C ABI, built with AddressSanitizer and
+// UndefinedBehaviorSanitizer on the host code (tests/test_host_sanitize.py).
+//
+// The library's host sources (argument validation, work planning, parameter
+// set-up, the Mode A budget) are linked against stub launchers that launch
+// nothing: they check the parameters the host code built -- the partial
+// arrays lie inside the caller's workspace, the work decomposition covers the
+// problem -- and report a launch failure, so every valid call must come back
+// as ZARYA_ERR_HIP with a message.  Device pointers are fake addresses that
+// nothing dereferences; no GPU is touched.
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <random>
+#include <vector>
+
+#include "kernels.hpp"
+#include "zarya.h"
+
+static int g_fail = 0;
+static int g_checks = 0;
+#define CHECK(c)                                                        \
+  do {                                                                  \
+    ++g_checks;                                                         \
+    if (!(c)) {                                                         \
+      std::printf("FAIL %s:%d: %s\n", __FILE__, __LINE__, #c);          \
+      ++g_fail;                                                         \
+    }                                                                   \
+  } while (0)
+
+// The fake workspace of the current call: [lo, hi).
+static uintptr_t g_ws_lo = 0, g_ws_hi = 0;
+static bool in_ws(const void* p, size_t bytes) {
+  const uintptr_t a = reinterpret_cast<uintptr_t>(p);
+  return a >= g_ws_lo && a + bytes <= g_ws_hi;
+}
+static int g_launches = 0;
+
+namespace zarya {
+
+hipError_t launch_slot_attn_bf16(const AttnParams& p, int head_dim, hipStream_t) {
+  ++g_launches;
+  CHECK(p.n_split >= 1 && p.n_split <= 64);
+  CHECK((int64_t)p.tiles_per_split * p.n_split >= p.n_prefix_tiles);
+  CHECK(p.n_split == 1 || (int64_t)p.tiles_per_split * (p.n_split - 1) < p.n_prefix_tiles);
+  CHECK((int64_t)p.n_rb * kAttnRowsPerBlock >= p.R && p.R == p.G * p.T);
+  CHECK(p.n_items == p.B * p.Hkv * p.n_split * p.n_rb);
+  CHECK(p.per_xcd * 8 >= p.n_items && (p.per_xcd - 1) * 8 < p.n_items);
+  if (p.n_split > 1) {
+    CHECK(in_ws(p.part_o, (size_t)p.n_split * p.rows_total * head_dim * 4));
+    CHECK(in_ws(p.part_lse, (size_t)p.n_split * p.rows_total * 4));
+    CHECK(reinterpret_cast<uintptr_t>(p.part_lse) >=
+          reinterpret_cast<uintptr_t>(p.part_o) + (size_t)p.n_split * p.rows_total * head_dim * 4);
+  }
+  return hipErrorNoDevice;
+}
+
+hipError_t launch_slot_attn_f32(const AttnParams32& p, int, hipStream_t) {
+  ++g_launches;
+  CHECK(p.rows_total == p.B * p.Hq * p.T);
+  return hipErrorNoDevice;
+}
+
+static void check_conf(const ConfParams& p) {
+  const size_t n = (size_t)p.n_vg * p.M * 4;
+  CHECK(in_ws(p.part_m, n) && in_ws(p.part_s, n) && in_ws(p.part_idx, n));
+  if (p.part_g) CHECK(in_ws(p.part_g, n) && in_ws(p.part_gi, n));
+  CHECK(p.n_vg >= 1);
+  CHECK(p.n_items == p.n_vg * p.n_rt);
+  CHECK(p.per_xcd * 8 >= p.n_items);
+  CHECK(p.row_index != nullptr || p.hidden_rows == p.M);
+}
+
+hipError_t launch_slot_conf_bf16(const ConfParams& p, hipStream_t) {
+  ++g_launches;
+  check_conf(p);
+  CHECK((int64_t)p.n_rt * conf_tile_rows(p.M) >= p.M);
+  CHECK(p.n_vg <= (p.V + 31) / 32);
+  return hipErrorNoDevice;
+}
+
+hipError_t launch_slot_conf_f32(const ConfParams& p, hipStream_t) {
+  ++g_launches;
+  check_conf(p);
+  CHECK(p.n_rt == 1 && p.n_vg <= 64);
+  return hipErrorNoDevice;
+}
+
+hipError_t launch_slot_conf_merge(const ConfMergeParams&, hipStream_t) { return hipErrorNoDevice; }
+
+hipError_t launch_select_slots(const SelectParams&, hipStream_t) {
+  ++g_launches;
+  return hipErrorNoDevice;
+}
+
+hipError_t launch_verify_accept(const AcceptParams& p, hipStream_t) {
+  ++g_launches;
+  CHECK(p.S >= 1 && p.S <= 1024 && p.L >= 1);
+  return hipErrorNoDevice;
+}
+
+hipError_t launch_kv_append(const AppendParams& p, hipStream_t) {
+  ++g_launches;
+  CHECK(p.row_bytes % 16 == 0 && p.S * p.L <= kAppendMaxTokens);
+  return hipErrorNoDevice;
+}
+
+hipError_t launch_mdm_reveal(const RevealParams& p, hipStream_t) {
+  ++g_launches;
+  CHECK(p.NP >= p.N && p.NP >= 2 && (p.NP & (p.NP - 1)) == 0 && p.NP <= kRevealMaxN);
+  CHECK(p.NP < 2 * p.N || p.NP == 2);
+  return hipErrorNoDevice;
+}
+
+}  // namespace zarya
+
+static void* fake(uintptr_t a) { return reinterpret_cast<void*>(a); }
+
+// A valid call must reach its launcher and report the launch failure.
+static void expect_launch(zarya_status st, int launches_before, const char* what) {
+  if (st != ZARYA_ERR_HIP || g_launches != launches_before + 1 || std::strlen(zarya_last_error()) == 0) {
+    std::printf("FAIL %s: status %s, launches %d -> %d\n", what, zarya_status_string(st), launches_before,
+                g_launches);
+    ++g_fail;
+  }
+  ++g_checks;
+}
+
+static void attn_cases(std::mt19937_64& rng) {
+  const int dims[2] = {64, 128};
+  for (int it = 0; it < 400; ++it) {
+    zarya_slot_attn_desc d{};
+    d.batch = 1 + (int)(rng() % 32);
+    d.n_kv_heads = 1 + (int)(rng() % 8);
+    d.n_q_heads = d.n_kv_heads * (1 + (int)(rng() % 4));
+    d.head_dim = dims[rng() % 2];
+    d.prefix_len = (rng() % 4 == 0) ? 0 : (int)(rng() % 20000);
+    d.kv_capacity = d.prefix_len + (int)(rng() % 300);
+    d.n_slots = 1 + (int)(rng() % 64);
+    d.slot_len = 1 + (int)(rng() % 32);
+    d.softmax_scale = 0.088f;
+    d.pass = (int)(rng() % 2);
+    d.cross_slot = (int)(rng() % 2);
+    d.dtype = (rng() % 5 == 0) ? ZARYA_DTYPE_F32 : ZARYA_DTYPE_BF16;
+    d.prefix_splits = (rng() % 3 == 0) ? (int)(rng() % 9) : 0;
+    size_t ws = 0;
+    CHECK(zarya_slot_attn_workspace_size(&d, &ws) == ZARYA_OK);
+    g_ws_lo = 0x100000000ull;
+    g_ws_hi = g_ws_lo + ws;
+    void* p = fake(0x200000000ull);
+    const int before = g_launches;
+    expect_launch(zarya_slot_attn(&d, p, p, p, p, p, nullptr, nullptr, p, nullptr, ws ? fake(g_ws_lo) : nullptr, ws,
+                                  nullptr),
+                  before, "slot_attn");
+    if (ws > 0) {
+      CHECK(zarya_slot_attn(&d, p, p, p, p, p, nullptr, nullptr, p, nullptr, fake(g_ws_lo), ws - 1, nullptr) ==
+            ZARYA_ERR_WORKSPACE_TOO_SMALL);
+    }
+  }
+}
+
+static void conf_cases(std::mt19937_64& rng) {
+  for (int it = 0; it < 400; ++it) {
+    zarya_conf_desc d{};
+    d.dtype = (rng() % 4 == 0) ? ZARYA_DTYPE_F32 : ZARYA_DTYPE_BF16;
+    d.n_rows = 1 + (int)(rng() % 5000);
+    d.hidden = 8 * (1 + (int)(rng() % 512));
+    d.vocab = 1 + (int)(rng() % 200000);
+    size_t ws = 0, ws_s = 0;
+    CHECK(zarya_slot_confidence_workspace_size(&d, &ws) == ZARYA_OK);
+    CHECK(zarya_slot_sample_workspace_size(&d, &ws_s) == ZARYA_OK && ws_s > ws);
+    void* p = fake(0x200000000ull);
+    g_ws_lo = 0x100000000ull;
+    g_ws_hi = g_ws_lo + ws;
+    int before = g_launches;
+    expect_launch(zarya_slot_confidence(&d, p, p, nullptr, (float*)p, (int32_t*)p, nullptr, nullptr, fake(g_ws_lo),
+                                        ws, nullptr),
+                  before, "slot_confidence");
+    CHECK(zarya_slot_confidence(&d, p, p, nullptr, (float*)p, (int32_t*)p, nullptr, nullptr, fake(g_ws_lo), ws - 1,
+                                nullptr) == ZARYA_ERR_WORKSPACE_TOO_SMALL);
+    g_ws_hi = g_ws_lo + ws_s;
+    zarya_sample_params sp{0.7f, 12345, 6};
+    const bool rows = rng() % 2 == 0;
+    before = g_launches;
+    expect_launch(zarya_slot_sample(&d, &sp, p, rows ? (const int32_t*)p : nullptr, rows ? 1 + (int)(rng() % 9000) : 0,
+                                    p, (int32_t*)p, (float*)p, nullptr, nullptr, fake(g_ws_lo), ws_s, nullptr),
+                  before, "slot_sample");
+  }
+}
+
+static void small_call_cases() {
+  void* p = fake(0x300000000ull);
+  int before = g_launches;
+  expect_launch(zarya_select_slots(4, 1024, 3, (const float*)p, nullptr, 1, 1, 0.9f, 5, (float*)p, (int32_t*)p,
+                                   (int32_t*)p, nullptr),
+                before, "select_slots");
+  before = g_launches;
+  expect_launch(zarya_verify_accept(4, 1024, 4096, (const float*)p, (const int32_t*)p, 0.4f, 0, (uint8_t*)p,
+                                    (int32_t*)p, nullptr, nullptr),
+                before, "verify_accept");
+  zarya_kv_append_desc a{2, 8, 128, 4096, 64, 128, ZARYA_DTYPE_BF16};
+  before = g_launches;
+  expect_launch(zarya_kv_append(&a, p, p, (const uint8_t*)p, (const int32_t*)p, (int32_t*)p, p, p, nullptr), before,
+                "kv_append");
+  for (int n : {1, 2, 3, 64, 65, 4097, 8192}) {
+    for (int rule = 0; rule < 3; ++rule) {
+      before = g_launches;
+      expect_launch(zarya_mdm_reveal(3, n, (const float*)p, (uint8_t*)p, (const int32_t*)p, rule, 1, 2, nullptr,
+                                     nullptr, (int32_t*)p, nullptr, nullptr),
+                    before, "mdm_reveal");
+    }
+  }
+  // rejected before any launch
+  before = g_launches;
+  CHECK(zarya_mdm_reveal(3, 8193, (const float*)p, (uint8_t*)p, (const int32_t*)p, 0, 1, 2, nullptr, nullptr,
+                         (int32_t*)p, nullptr, nullptr) == ZARYA_ERR_UNSUPPORTED);
+  CHECK(zarya_select_slots(4, 1025, 3, (const float*)p, nullptr, 0, 0, 0.9f, 1, (float*)p, (int32_t*)p, (int32_t*)p,
+                           nullptr) == ZARYA_ERR_UNSUPPORTED);
+  zarya_kv_append_desc big{2, 8, 128, 4096, 512, 32, ZARYA_DTYPE_BF16};
+  CHECK(zarya_kv_append(&big, p, p, (const uint8_t*)p, (const int32_t*)p, (int32_t*)p, p, p, nullptr) ==
+        ZARYA_ERR_UNSUPPORTED);
+  CHECK(g_launches == before);
+}
+
+// The plan is written into a buffer of exactly the reported length, so any
+// write past it is caught by the sanitizer.
+static void budget_cases(std::mt19937_64& rng) {
+  for (int it = 0; it < 300; ++it) {
+    const int n = (int)(rng() % 3000);
+    const int t = (int)(rng() % 40);
+    const double a = (double)(rng() % 1001) / 1000.0;
+    const uint64_t seed = rng();
+    int32_t len = -1, diff = -1;
+    CHECK(zarya_mdm_budget(n, t, a, seed, nullptr, 0, &len, &diff) == ZARYA_OK);
+    std::vector<int32_t>* buf = new std::vector<int32_t>((size_t)len);
+    int32_t len2 = -1;
+    CHECK(zarya_mdm_budget(n, t, a, seed, buf->data(), len, &len2, &diff) == ZARYA_OK && len2 == len);
+    long long sum = 0;
+    for (int32_t c : *buf) sum += c;
+    CHECK(sum == n);
+    CHECK(diff == (n == 0 ? 0 : (t > 0 ? t : (n + 3) / 4)));
+    if (len > 0) CHECK(zarya_mdm_budget(n, t, a, seed, buf->data(), len - 1, &len2, &diff) == ZARYA_ERR_INVALID_ARGUMENT);
+    delete buf;
+  }
+}
+
+int main() {
+  std::mt19937_64 rng(20260);
+  attn_cases(rng);
+  conf_cases(rng);
+  small_call_cases();
+  budget_cases(rng);
+  std::printf("%d checks, %d failures, %d launches reached\n", g_checks, g_fail, g_launches);
+  return g_fail == 0 ? 0 : 1;
+}
