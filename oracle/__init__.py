@@ -13,7 +13,8 @@ Language Model with Flexible Training and Dual-Mode Inference"):
   against a reused prefix KV cache (Sec. 5.1 KV-reuse argument, Sec. 5.2
   draft and verification phases, Sec. 3.1 causal masked reconstruction).
 * ``confidence``  -- full-vocabulary softmax statistics of the LM head
-  (Sec. 5.2 "probability of its first token", Table 1 tied embedding).
+  (Sec. 5.2: a slot's confidence is its first token's probability; Table 1
+  tied embedding).
 * ``selection``   -- slot confidence and first-hitting slot selection
   (Sec. 5.2 slot selection, Sec. 6 inference settings).
 * ``sampling``    -- Gumbel-max sampling with temperature from a Philox4x32-10
