@@ -90,6 +90,7 @@ SMALL = [
     ("m513_v33000_h1024", dict(batch=1, n_slots=27, slot_len=19, hidden=1024, vocab=33000)),
     ("m128_v7001_h512", dict(batch=1, n_slots=16, slot_len=8, hidden=512, vocab=7001)),  # largest 64-row-tile case
     ("m129_v7001_h512", dict(batch=1, n_slots=43, slot_len=3, hidden=512, vocab=7001)),  # smallest 256-row-tile case
+    ("m3_v1_h8", dict(batch=1, n_slots=3, slot_len=1, hidden=8, vocab=1)),  # a one-token vocabulary
 ]
 
 

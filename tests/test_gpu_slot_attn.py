@@ -55,6 +55,9 @@ SMALL_BF16 = [
     ("l1_decode", dict(batch=2, n_q_heads=4, n_kv_heads=4, prefix_len=130, n_slots=16, slot_len=1)),
     ("one_slot", dict(batch=1, n_q_heads=4, n_kv_heads=1, prefix_len=64, n_slots=1, slot_len=33)),
     ("d64", dict(batch=2, n_q_heads=4, n_kv_heads=2, head_dim=64, prefix_len=257, n_slots=4, slot_len=6)),
+    # one key past a tile, and slots longer than several key tiles
+    ("p65_long_slots", dict(batch=1, n_q_heads=2, n_kv_heads=1, prefix_len=65, n_slots=2, slot_len=200)),
+    ("p1", dict(batch=3, n_q_heads=2, n_kv_heads=2, prefix_len=1, n_slots=3, slot_len=4)),
 ]
 
 
