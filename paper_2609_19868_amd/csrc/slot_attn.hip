@@ -39,6 +39,7 @@ namespace zarya {
 namespace {
 
 constexpr int KT = 64;          // keys per tile
+constexpr float kRescaleLog2 = 8.f;  // growth of a row maximum (log2 units) that forces a rescale
 constexpr int NWAVE = 4;        // waves per workgroup
 constexpr int RB = NWAVE * 32;  // query rows per workgroup
 
@@ -288,7 +289,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(ZARYA_ATTN_
     mt = max3f(mt, sacc[1][15], sacc[1][15]);
     mt = fmaxf(mt, __shfl_xor(mt, 32));
     const float m_new = fmaxf(m_run, mt);
-    if (__any(m_new > m_run)) {  // the running maximum moved for some row: rescale
+    // Rescale only when the maximum of some row moved by more than 2^8 in
+    // probability: until then the exponentials below are taken against the
+    // stale maximum and stay <= 2^8 (exact in the float32 sums, same relative
+    // rounding in bf16), and the final O / l and LSE do not depend on which
+    // maximum was used.  Random scores raise a row's maximum on most early
+    // tiles, each time by little; this skips those rescales.
+    if (__any((m_new - m_run) * c2 > kRescaleLog2)) {
       const float alpha = fast_exp2((m_run - m_new) * c2);
       l_run *= alpha;
 #pragma unroll
