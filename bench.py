@@ -269,6 +269,8 @@ def main():
     }
 
     if not args.no_extras:
+        log("timing the same step replayed from HIP graphs")
+        result["graph_step"] = graph_step(step, sets, args.steps)
         log("timing the AR_INFILL (verification) pass")
         ms_ar, mean_ar, _, _ = timed(Z.PASS_AR_INFILL, max(10, args.steps // 2), 3)
         result["ar_infill_pass"] = {"steps_per_s": 1e3 / ms_ar, "slot_attn_us": mean_ar[0] * 1e3}
@@ -289,6 +291,39 @@ def main():
         log("timing the float64 CPU oracle (reference baseline)")
         result["cpu_baseline"] = cpu_baseline(wl, x, c)
     print(json.dumps(result), flush=True)
+
+
+def graph_step(step, sets, K):
+    """The scoring step captured once per input copy in a HIP graph
+    (torch.cuda.CUDAGraph over the library's launches) and replayed: the same
+    kernels without the host-side launch path between them."""
+    import torch
+
+    import paper_2609_19868_amd as Z
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for s in sets:
+            step(s, Z.PASS_DIFFUSION)
+    torch.cuda.current_stream().wait_stream(side)
+    graphs = []
+    for s in sets:
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            step(s, Z.PASS_DIFFUSION)
+        graphs.append(g)
+    for g in graphs:
+        g.replay()
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for i in range(K):
+        graphs[i % len(graphs)].replay()
+    t1.record()
+    torch.cuda.synchronize()
+    us = t0.elapsed_time(t1) / K * 1e3
+    return {"step_us": us, "steps_per_s": 1e6 / us}
 
 
 def verification_step(dev, wl, s, conf_out, sel_out, K):
