@@ -120,18 +120,23 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(AppendParams p) {
   const int T = p.S * p.L;
   const int pieces = p.row_bytes / 16;
   const int n = n_tok;
-  for (int g = 0; g < p.Hkv; ++g) {
-    const size_t src_base = ((size_t)b * p.Hkv + g) * T;
-    const size_t dst_base = ((size_t)b * p.Hkv + g) * p.C + p0;
-    for (int e = tid; e < n * pieces; e += kThreads) {
-      const int i = e / pieces, c = e - i * pieces;
-      const size_t src = (src_base + tokens[i]) * p.row_bytes + (size_t)c * 16;
-      const size_t dst = (dst_base + i) * p.row_bytes + (size_t)c * 16;
-      *reinterpret_cast<uint4*>(static_cast<char*>(p.k_cache) + dst) =
-          *reinterpret_cast<const uint4*>(static_cast<const char*>(p.k_slot) + src);
-      *reinterpret_cast<uint4*>(static_cast<char*>(p.v_cache) + dst) =
-          *reinterpret_cast<const uint4*>(static_cast<const char*>(p.v_slot) + src);
-    }
+  // one flat loop over (head, token, 16-byte piece): every thread's loads are
+  // independent of its stores (the slot K/V and the cache never overlap), so
+  // many are in flight at once
+  const char* __restrict__ ks = static_cast<const char*>(p.k_slot);
+  const char* __restrict__ vs = static_cast<const char*>(p.v_slot);
+  char* __restrict__ kc = static_cast<char*>(p.k_cache);
+  char* __restrict__ vc = static_cast<char*>(p.v_cache);
+  const int per_head = n * pieces;
+  for (int e = tid; e < p.Hkv * per_head; e += kThreads) {
+    const int g = e / per_head, r = e - g * per_head;
+    const int i = r / pieces, c = r - i * pieces;
+    const size_t src = (((size_t)b * p.Hkv + g) * T + tokens[i]) * p.row_bytes + (size_t)c * 16;
+    const size_t dst = (((size_t)b * p.Hkv + g) * p.C + p0 + i) * p.row_bytes + (size_t)c * 16;
+    const uint4 kv = *reinterpret_cast<const uint4*>(ks + src);
+    const uint4 vv = *reinterpret_cast<const uint4*>(vs + src);
+    *reinterpret_cast<uint4*>(kc + dst) = kv;
+    *reinterpret_cast<uint4*>(vc + dst) = vv;
   }
   if (tid == 0) p.prefix_lens[b] = p0 + n;
 }
