@@ -336,9 +336,24 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
     const int xr = conf_hidden_row(p.row_index, p.hidden_rows, min(row0 + r, p.M - 1));
     b_off[j] = (uint32_t)((size_t)xr * H + b_col[j]) * 2u;
   }
+  // Stage cursors: (vocab tile, k-stage, ring slot) of the next W and hidden
+  // stage to load and of the stage being consumed, advanced by one stage at a
+  // time (no integer division in the loop).
+  struct Cursor {
+    int st, vt, kq, slot;
+  };
+  auto advance = [&](Cursor& c, int ring) {
+    ++c.st;
+    if (++c.kq == nks) {
+      c.kq = 0;
+      ++c.vt;
+    }
+    if (++c.slot == ring) c.slot = 0;
+  };
+  Cursor cw{0, 0, 0, 0}, cx{0, 0, 0, 0};
   int cur_vt = -1;
-  auto issue_w = [&](int st) {
-    const int vt = st / nks, kk = (st - vt * nks) * BK;
+  auto issue_w = [&]() {  // the W tile of stage cw.st
+    const int vt = cw.vt, kk = cw.kq * BK;
     const int vb = v_lo + vt * BV;
     if (vt != cur_vt) {
 #pragma unroll
@@ -347,7 +362,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
       cur_vt = vt;
     }
     const char* base = reinterpret_cast<const char*>(W + (size_t)vb * H + kk);
-    uint8_t* dst = &lds_w[st % NSW][wave_u * 1024];
+    uint8_t* dst = &lds_w[cw.slot][wave_u * 1024];
     if (!k_ragged || kk + BK <= H) {
 #pragma unroll
       for (int j = 0; j < CPA; ++j) dma16(base + a_off[j], dst + NW * j * 1024);
@@ -358,11 +373,12 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
         dma16(base + a_off[j] + 2 * dk, dst + NW * j * 1024);
       }
     }
+    advance(cw, NSW);
   };
-  auto issue_x = [&](int st) {
-    const int kk = (st % nks) * BK;
+  auto issue_x = [&]() {  // the hidden tile of stage cx.st
+    const int kk = cx.kq * BK;
     const char* base = reinterpret_cast<const char*>(X + kk);
-    uint8_t* dst = &lds_x[st % NSX][wave_u * 1024];
+    uint8_t* dst = &lds_x[cx.slot][wave_u * 1024];
     if (!k_ragged || kk + BK <= H) {
 #pragma unroll
       for (int j = 0; j < CPB; ++j) dma16(base + b_off[j], dst + NW * j * 1024);
@@ -373,17 +389,19 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
         dma16(base + b_off[j] + 2 * dk, dst + NW * j * 1024);
       }
     }
+    advance(cx, NSX);
   };
-  auto zero_k_tail = [&](int st) {
-    const int kk = (st % nks) * BK;
+  auto zero_k_tail = [&](const Cursor& c) {
+    const int kk = c.kq * BK;
+    const int sw = c.st % NSW, sx = c.st % NSX;
 #pragma unroll
     for (int j = 0; j < CPA; ++j)
       if (kk + a_col[j] >= H)
-        *reinterpret_cast<uint4*>(&lds_w[st % NSW][(NW * j + wave) * 1024 + lane * 16]) = make_uint4(0, 0, 0, 0);
+        *reinterpret_cast<uint4*>(&lds_w[sw][(NW * j + wave) * 1024 + lane * 16]) = make_uint4(0, 0, 0, 0);
 #pragma unroll
     for (int j = 0; j < CPB; ++j)
       if (kk + b_col[j] >= H)
-        *reinterpret_cast<uint4*>(&lds_x[st % NSX][(NW * j + wave) * 1024 + lane * 16]) = make_uint4(0, 0, 0, 0);
+        *reinterpret_cast<uint4*>(&lds_x[sx][(NW * j + wave) * 1024 + lane * 16]) = make_uint4(0, 0, 0, 0);
   };
 
   f32x16 acc[IB][JB];  // set by the first k-step of every vocab tile
@@ -404,35 +422,47 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
   // W tile of stage i+NSW-1; the prologue issues what iterations before 0
   // would have.  Loads complete in issue order, so when the hidden tile of
   // stage i has landed so has its W tile, and with NSW = 3 only the W tile of
-  // stage i+1 (CPA loads) may still be in flight.
+  // stage i+1 (CPA loads) may still be in flight.  Waves with work issue the W
+  // tile after the MFMAs of the stage's first k-step, so that its address
+  // arithmetic runs while the matrix pipe is busy.
   for (int j = -(NSW - 1); j < 0; ++j) {
-    if (j + NSX - 1 >= 0 && j + NSX - 1 < n_st) issue_x(j + NSX - 1);
-    if (j + NSW - 1 < n_st) issue_w(j + NSW - 1);
+    if (j + NSX - 1 >= 0 && cx.st < n_st) issue_x();
+    if (cw.st < n_st) issue_w();
   }
 
+  // The kernel arguments' scalar loads have all landed: without this the
+  // compiler, which cannot see the LDS waits in inline assembly, re-waits for
+  // them (lgkmcnt(0), also draining the fragment reads) inside the loop.
+  __builtin_amdgcn_s_waitcnt(0xc07f);
+  Cursor cc{0, 0, 0, 0};  // the stage consumed by this iteration (slot: W ring)
+  int sx_c = 0;           // its slot in the hidden ring
   for (int i = 0; i < n_st; ++i) {
     if (NSW == 3 && i + 1 < n_st) {
       wait_vmcnt<CPA>();
     } else {
       wait_vmcnt<0>();
     }
-    if (k_ragged && (i % nks) == nks - 1) zero_k_tail(i);
+    if (k_ragged && cc.kq == nks - 1) zero_k_tail(cc);
     block_barrier();
     // the buffers consumed in the previous iteration are free
-    if (i + NSX - 1 < n_st) issue_x(i + NSX - 1);
-    if (i + NSW - 1 < n_st) issue_w(i + NSW - 1);
+    if (cx.st < n_st) issue_x();
+    const bool load_w = cw.st < n_st;
 
-    const int vt = i / nks;
-    const int vbase = v_lo + vt * BV + wv * 128;  // first vocab id of this wave's half
+    const int vt = cc.vt;
+    // first vocab id of this wave's half, from the wave index in a scalar
+    // register so that `active` (and the stage cursors updated under it) stays
+    // wave-uniform for the compiler
+    const int vbase = v_lo + vt * BV + (wave_u & 1) * 128;
     const bool active = vbase < v_hi;
-    const bool fresh = i % nks == 0;
+    const bool fresh = cc.kq == 0;
+    if (!active && load_w) issue_w();
     if (active) {
       // Operand fragments are double-buffered across k-steps: the LDS reads of
       // step ks+1 are issued before the MFMAs of step ks, which wait only for
       // their own reads.  The swizzle of every row a lane reads depends on the
       // lane alone, so one base address per step plus immediate offsets
       // address all fragments of that step.
-      const uint32_t wsb = lds_addr(lds_w[i % NSW]), xsb = lds_addr(lds_x[i % NSX]);
+      const uint32_t wsb = lds_addr(lds_w[cc.slot]), xsb = lds_addr(lds_x[sx_c]);
       bf16x8 a[2][IB], bfr[2][JB];
       auto frag_load = [&](int ks, int sl) {
         const uint32_t col = ((2 * ks + hh) ^ cswz<BK>(n)) << 4;
@@ -475,15 +505,21 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
         }
         // keep this step's MFMAs ahead of the next step's reads and waits
         __builtin_amdgcn_sched_barrier(0);
+        if (ks == 0 && load_w) {
+          issue_w();
+          __builtin_amdgcn_sched_barrier(0);
+        }
       }
     }
-    if (i % nks == nks - 1) {
+    if (cc.kq == nks - 1) {
       if (active) {
         fold_tile<JB, !SAMPLE>(acc, v_hi - vbase - 4 * hh, vbase + 4 * hh, m_run, s_run, i_run);
         if constexpr (SAMPLE)
           sample_fold<JB>(acc, v_hi - vbase - 4 * hh, vbase + 4 * hh, row0 + rbase + n, p, g_best, g_id);
       }
     }
+    advance(cc, NSW);
+    if (++sx_c == NSX) sx_c = 0;
   }
   block_barrier();  // every wave is done with the stage buffers (reused below)
   store_partials<JB, BR, SAMPLE>(p, vg, row0, rbase, wv, hh, n, m_run, s_run, i_run, g_best, g_id, &lds_w[0][0]);
