@@ -49,6 +49,21 @@ __device__ __forceinline__ void dma16(const void* src, void* lds_base) {
   __builtin_amdgcn_global_load_lds(src, (lds_ptr)lds_base, 16, 0, 0);
 }
 
+// Buffer resource of `bytes` (< 4 GiB) bytes at `base` for raw byte-offset
+// loads (stride 0; loads past the end return zeros).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+// Direct buffer->LDS copy of 16 bytes per lane: lane l reads the bytes at
+// byte offset voffset + soffset of `rsrc` and writes them to LDS at
+// lds_base + 16*l (lds_base wave-uniform).  Addresses are 32-bit offsets, so
+// no 64-bit address arithmetic per load.
+__device__ __forceinline__ void dmab16(__amdgpu_buffer_rsrc_t rsrc, void* lds_base, uint32_t voffset,
+                                       uint32_t soffset) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_ptr)lds_base, 16, voffset, soffset, 0, 0);
+}
+
 // Wait until at most N vector-memory operations of this wave are in flight
 // (direct global->LDS loads count until their data is in LDS).
 template <int N>

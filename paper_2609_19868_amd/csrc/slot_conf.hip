@@ -309,32 +309,29 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
   // Direct-to-LDS staging: load j of a wave fills 1 KB chunk c = NW*j + wave
   // of an operand tile; lane l lands at byte 16*l of it, i.e. row RPC*c + l/LPR
   // and physical column l%LPR, and fetches the logical column the swizzle puts
-  // there.  Rows past the vocabulary range or the row count are clamped to a
-  // valid row (their results are masked or never stored); columns past H are
-  // clamped and zeroed in LDS before use.
+  // there.  The swizzle repeats every 16 rows and chunk j starts RPC*NW*j rows
+  // after chunk 0, so a lane's column is the same in every chunk.  W rows are
+  // read through a buffer resource covering the current vocab tile's rows:
+  // chunk j is chunk 0 moved by a scalar offset, and rows past the vocabulary
+  // fall outside the buffer (read as zeros; their logits are masked).  Hidden
+  // rows past the row count are clamped to a valid row (never stored); columns
+  // past H are clamped and zeroed in LDS before use.
   const int nks = (H + BK - 1) / BK;
   const int n_st = n_vt * nks;
   const bool k_ragged = (H % BK) != 0;
   const int lcol = lane % LPR, lrow = lane / LPR;
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);  // wave index in a scalar register
-  // Per-lane byte offsets of the bytes this lane fetches, relative to a
-  // wave-uniform base that only moves with the stage: fixed for the whole
-  // hidden tile, and for a vocab tile of W (recomputed when the tile changes,
-  // which also applies the row clamp of the last tile).
-  int a_r[CPA], a_col[CPA];
-  uint32_t a_off[CPA], b_off[CPB];
-  int b_col[CPB];
-#pragma unroll
-  for (int j = 0; j < CPA; ++j) {
-    a_r[j] = RPC * (NW * j + wave_u) + lrow;
-    a_col[j] = 8 * (lcol ^ cswz<BK>(a_r[j]));
-  }
+  static_assert((RPC * NW) % 16 == 0, "chunks must keep the swizzle phase");
+  const int l_row = RPC * wave_u + lrow;                        // row of this lane in chunk 0
+  const int l_col = 8 * (lcol ^ cswz<BK>(l_row));               // its logical column, every chunk
+  const uint32_t a_off = (uint32_t)(l_row * H + l_col) * 2u;    // in the W tile, chunk 0
+  const uint32_t a_step = (uint32_t)(RPC * NW) * (uint32_t)H * 2u;  // bytes from chunk j to j+1
+  uint32_t b_off[CPB];  // in the hidden states, per chunk (rows may be gathered)
 #pragma unroll
   for (int j = 0; j < CPB; ++j) {
-    const int r = RPC * (NW * j + wave_u) + lrow;
-    b_col[j] = 8 * (lcol ^ cswz<BK>(r));
+    const int r = l_row + RPC * NW * j;
     const int xr = conf_hidden_row(p.row_index, p.hidden_rows, min(row0 + r, p.M - 1));
-    b_off[j] = (uint32_t)((size_t)xr * H + b_col[j]) * 2u;
+    b_off[j] = (uint32_t)((size_t)xr * H + l_col) * 2u;
   }
   // Stage cursors: (vocab tile, k-stage, ring slot) of the next W and hidden
   // stage to load and of the stage being consumed, advanced by one stage at a
@@ -352,56 +349,42 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
   };
   Cursor cw{0, 0, 0, 0}, cx{0, 0, 0, 0};
   int cur_vt = -1;
+  __amdgpu_buffer_rsrc_t rsrc_w = buffer_rsrc(W, 0);  // the current vocab tile's rows of W
+  const __amdgpu_buffer_rsrc_t rsrc_x =
+      buffer_rsrc(X, (uint32_t)((size_t)(p.row_index ? p.hidden_rows : p.M) * H * 2));
+  // byte shift of this lane's column in the last, partial k-stage, whose
+  // columns past H are clamped (and zeroed in LDS before use)
+  auto ragged_shift = [&](int kk) { return 2 * (min(kk + l_col, H - 8) - (kk + l_col)); };
   auto issue_w = [&]() {  // the W tile of stage cw.st
     const int vt = cw.vt, kk = cw.kq * BK;
-    const int vb = v_lo + vt * BV;
     if (vt != cur_vt) {
-#pragma unroll
-      for (int j = 0; j < CPA; ++j)
-        a_off[j] = (uint32_t)((size_t)(min(vb + a_r[j], p.V - 1) - vb) * H + a_col[j]) * 2u;
+      const int vb = v_lo + vt * BV;
+      rsrc_w = buffer_rsrc(W + (size_t)vb * H, (uint32_t)((size_t)(min(p.V, vb + BV) - vb) * H * 2));
       cur_vt = vt;
     }
-    const char* base = reinterpret_cast<const char*>(W + (size_t)vb * H + kk);
     uint8_t* dst = &lds_w[cw.slot][wave_u * 1024];
-    if (!k_ragged || kk + BK <= H) {
+    const uint32_t off = (!k_ragged || kk + BK <= H) ? a_off : a_off + ragged_shift(kk);
 #pragma unroll
-      for (int j = 0; j < CPA; ++j) dma16(base + a_off[j], dst + NW * j * 1024);
-    } else {  // the last, partial k-stage: clamp the columns past H (zeroed before use)
-#pragma unroll
-      for (int j = 0; j < CPA; ++j) {
-        const int dk = min(kk + a_col[j], H - 8) - (kk + a_col[j]);
-        dma16(base + a_off[j] + 2 * dk, dst + NW * j * 1024);
-      }
-    }
+    for (int j = 0; j < CPA; ++j) dmab16(rsrc_w, dst + NW * j * 1024, off, 2u * kk + j * a_step);
     advance(cw, NSW);
   };
   auto issue_x = [&]() {  // the hidden tile of stage cx.st
     const int kk = cx.kq * BK;
-    const char* base = reinterpret_cast<const char*>(X + kk);
     uint8_t* dst = &lds_x[cx.slot][wave_u * 1024];
-    if (!k_ragged || kk + BK <= H) {
+    const int dk = (!k_ragged || kk + BK <= H) ? 0 : ragged_shift(kk);
 #pragma unroll
-      for (int j = 0; j < CPB; ++j) dma16(base + b_off[j], dst + NW * j * 1024);
-    } else {
-#pragma unroll
-      for (int j = 0; j < CPB; ++j) {
-        const int dk = min(kk + b_col[j], H - 8) - (kk + b_col[j]);
-        dma16(base + b_off[j] + 2 * dk, dst + NW * j * 1024);
-      }
-    }
+    for (int j = 0; j < CPB; ++j) dmab16(rsrc_x, dst + NW * j * 1024, b_off[j] + dk, 2u * kk);
     advance(cx, NSX);
   };
   auto zero_k_tail = [&](const Cursor& c) {
-    const int kk = c.kq * BK;
+    if (c.kq * BK + l_col < H) return;  // this lane's column is inside H in every chunk
     const int sw = c.st % NSW, sx = c.st % NSX;
 #pragma unroll
     for (int j = 0; j < CPA; ++j)
-      if (kk + a_col[j] >= H)
-        *reinterpret_cast<uint4*>(&lds_w[sw][(NW * j + wave) * 1024 + lane * 16]) = make_uint4(0, 0, 0, 0);
+      *reinterpret_cast<uint4*>(&lds_w[sw][(NW * j + wave) * 1024 + lane * 16]) = make_uint4(0, 0, 0, 0);
 #pragma unroll
     for (int j = 0; j < CPB; ++j)
-      if (kk + b_col[j] >= H)
-        *reinterpret_cast<uint4*>(&lds_x[sx][(NW * j + wave) * 1024 + lane * 16]) = make_uint4(0, 0, 0, 0);
+      *reinterpret_cast<uint4*>(&lds_x[sx][(NW * j + wave) * 1024 + lane * 16]) = make_uint4(0, 0, 0, 0);
   };
 
   f32x16 acc[IB][JB];  // set by the first k-step of every vocab tile
