@@ -58,7 +58,9 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, 
 // Direct buffer->LDS copy of 16 bytes per lane: lane l reads the bytes at
 // byte offset voffset + soffset of `rsrc` and writes them to LDS at
 // lds_base + 16*l (lds_base wave-uniform).  Addresses are 32-bit offsets, so
-// no 64-bit address arithmetic per load.
+// no 64-bit address arithmetic per load.  Only voffset is checked against the
+// buffer's size (soffset is not): an access whose voffset is past the end
+// reads zeros, while one whose soffset carries it past the end is not caught.
 __device__ __forceinline__ void dmab16(__amdgpu_buffer_rsrc_t rsrc, void* lds_base, uint32_t voffset,
                                        uint32_t soffset) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_ptr)lds_base, 16, voffset, soffset, 0, 0);

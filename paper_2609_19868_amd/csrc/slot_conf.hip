@@ -312,8 +312,11 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
   // there.  The swizzle repeats every 16 rows and chunk j starts RPC*NW*j rows
   // after chunk 0, so a lane's column is the same in every chunk.  W rows are
   // read through a buffer resource covering the current vocab tile's rows:
-  // chunk j is chunk 0 moved by a scalar offset, and rows past the vocabulary
-  // fall outside the buffer (read as zeros; their logits are masked).  Hidden
+  // chunk j is chunk 0 moved by a_step bytes, and rows past the vocabulary
+  // fall outside the buffer and read as zeros (their logits are masked).  The
+  // row offset is part of the per-lane offset, which the hardware checks
+  // against the buffer's size; the scalar offset (the stage's k column) is not
+  // checked and stays inside a row.  Hidden
   // rows past the row count are clamped to a valid row (never stored); columns
   // past H are clamped and zeroed in LDS before use.
   const int nks = (H + BK - 1) / BK;
@@ -365,7 +368,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
     uint8_t* dst = &lds_w[cw.slot][wave_u * 1024];
     const uint32_t off = (!k_ragged || kk + BK <= H) ? a_off : a_off + ragged_shift(kk);
 #pragma unroll
-    for (int j = 0; j < CPA; ++j) dmab16(rsrc_w, dst + NW * j * 1024, off, 2u * kk + j * a_step);
+    for (int j = 0; j < CPA; ++j) dmab16(rsrc_w, dst + NW * j * 1024, off + j * a_step, 2u * kk);
     advance(cw, NSW);
   };
   auto issue_x = [&]() {  // the hidden tile of stage cx.st
