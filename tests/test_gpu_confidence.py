@@ -59,6 +59,9 @@ SMALL = [
     ("m128_v7001_h512", dict(batch=1, n_slots=16, slot_len=8, hidden=512, vocab=7001)),  # largest 64-row-tile case
     ("m129_v7001_h512", dict(batch=1, n_slots=43, slot_len=3, hidden=512, vocab=7001)),  # smallest 256-row-tile case
     ("m3_v1_h8", dict(batch=1, n_slots=3, slot_len=1, hidden=8, vocab=1)),  # a one-token vocabulary
+    # 256-row tile with a partial last k-stage (200 = 3*64 + 8) and last vocab tiles of a few rows
+    ("m260_v3001_h200", dict(batch=1, n_slots=52, slot_len=5, hidden=200, vocab=3001)),
+    ("m257_v257_h72", dict(batch=1, n_slots=257, slot_len=1, hidden=72, vocab=257)),
 ]
 
 
