@@ -394,30 +394,55 @@ __global__ __launch_bounds__(256) void slot_attn_merge_kernel(const float* __res
                                                               const float* __restrict__ part_lse, int n_split,
                                                               int rows_total, uint16_t* __restrict__ out,
                                                               float* __restrict__ lse) {
-  constexpr int PER = D / 64;
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  // a lane merges 4 consecutive elements of one row: D/4 lanes per row
+  constexpr int LPR = D / 4, RPW = 64 / LPR;
+  constexpr int MAXS = 8;  // splits whose loads are all issued before any arithmetic
   const int lane = threadIdx.x & 63;
+  const int row = (blockIdx.x * 4 + (threadIdx.x >> 6)) * RPW + lane / LPR;
+  const int c = (lane % LPR) * 4;
   if (row >= rows_total) return;
+  float l[MAXS];
+  float4 o[MAXS];
+  const int ns = min(n_split, MAXS);
+#pragma unroll
+  for (int i = 0; i < MAXS; ++i) {  // every load in flight at once
+    if (i < ns) {
+      l[i] = part_lse[(size_t)i * rows_total + row];
+      o[i] = *reinterpret_cast<const float4*>(part_o + ((size_t)i * rows_total + row) * D + c);
+    }
+  }
   float mx = -INFINITY;
-  for (int i = 0; i < n_split; ++i) mx = fmaxf(mx, part_lse[(size_t)i * rows_total + row]);
-  float acc[PER] = {};
+#pragma unroll
+  for (int i = 0; i < MAXS; ++i)
+    if (i < ns) mx = fmaxf(mx, l[i]);
+  for (int i = MAXS; i < n_split; ++i) mx = fmaxf(mx, part_lse[(size_t)i * rows_total + row]);
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
   float wsum = 0.f;
-  for (int i = 0; i < n_split; ++i) {
+#pragma unroll
+  for (int i = 0; i < MAXS; ++i) {
+    if (i < ns) {
+      const float wi = l[i] == -INFINITY ? 0.f : fast_exp2(l[i] - mx);
+      wsum += wi;
+      acc[0] += wi * o[i].x;
+      acc[1] += wi * o[i].y;
+      acc[2] += wi * o[i].z;
+      acc[3] += wi * o[i].w;
+    }
+  }
+  for (int i = MAXS; i < n_split; ++i) {
     const float li = part_lse[(size_t)i * rows_total + row];
     const float wi = li == -INFINITY ? 0.f : fast_exp2(li - mx);
     wsum += wi;
-    const float* po = part_o + ((size_t)i * rows_total + row) * D + lane * PER;
-#pragma unroll
-    for (int e = 0; e < PER; ++e) acc[e] += wi * po[e];
+    const float4 oi = *reinterpret_cast<const float4*>(part_o + ((size_t)i * rows_total + row) * D + c);
+    acc[0] += wi * oi.x;
+    acc[1] += wi * oi.y;
+    acc[2] += wi * oi.z;
+    acc[3] += wi * oi.w;
   }
   const float inv = 1.f / wsum;
-  uint16_t* orow = out + (size_t)row * D + lane * PER;
-  if constexpr (PER == 2) {
-    *reinterpret_cast<uint32_t*>(orow) = pack_bf16x2_hw(acc[0] * inv, acc[1] * inv);
-  } else {
-    orow[0] = f32_to_bf16(acc[0] * inv);
-  }
-  if (lse && lane == 0) lse[row] = (mx + __log2f(wsum)) * kLn2;
+  *reinterpret_cast<uint2*>(out + (size_t)row * D + c) =
+      make_uint2(pack_bf16x2_hw(acc[0] * inv, acc[1] * inv), pack_bf16x2_hw(acc[2] * inv, acc[3] * inv));
+  if (lse && c == 0) lse[row] = (mx + __log2f(wsum)) * kLn2;
 }
 
 // float32 path: one thread per query row, plain FMA arithmetic, online softmax
@@ -478,7 +503,8 @@ hipError_t launch_slot_attn_bf16(const AttnParams& p, int head_dim, hipStream_t 
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.n_split == 1) return e;
-  const int mgrid = (p.rows_total + 3) / 4;
+  const int rows_per_wg = 4 * (64 / (head_dim / 4));  // four waves, 64 / (D/4) rows each
+  const int mgrid = (p.rows_total + rows_per_wg - 1) / rows_per_wg;
   if (head_dim == 128) {
     hipLaunchKernelGGL(slot_attn_merge_kernel<128>, dim3(mgrid), dim3(256), 0, stream, p.part_o, p.part_lse,
                        p.n_split, p.rows_total, p.out, p.lse);
