@@ -612,6 +612,10 @@ __global__ __launch_bounds__(256) void slot_conf_merge_kernel(ConfMergeParams p)
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (row >= p.M) return;
+  // loads that do not depend on the partials go first, so that their latency
+  // overlaps the partials' (the target logit needs the target id)
+  const int tgt = p.target_ids ? p.target_ids[row] : -1;
+  const int hrow = conf_hidden_row(p.row_index, p.hidden_rows, row);
   float m = kNegBig, s = 0.f;
   int idx = INT_MAX;
   float sg = -INFINITY;
@@ -634,9 +638,7 @@ __global__ __launch_bounds__(256) void slot_conf_merge_kernel(ConfMergeParams p)
     }
   }
   const float lse2 = m * kLog2e + __log2f(s);
-  const int tgt = p.target_ids ? p.target_ids[row] : -1;
   const bool tgt_ok = tgt >= 0 && tgt < p.V;
-  const int hrow = conf_hidden_row(p.row_index, p.hidden_rows, row);
   const float zt = tgt_ok ? row_logit(p, hrow, tgt, lane) : 0.f;
   // every row has a finite perturbed score, so sgi is a valid id
   const float zs = p.part_g ? row_logit(p, hrow, sgi, lane) : 0.f;
