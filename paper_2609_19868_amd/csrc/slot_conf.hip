@@ -64,11 +64,6 @@ __device__ __forceinline__ int cswz(int r) {
   }
 }
 
-template <int BK>
-__device__ __forceinline__ int coff(int r, int ch) {
-  return r * (BK * 2) + ((ch ^ cswz<BK>(r)) << 4);
-}
-
 }  // namespace
 
 // Fold one vocab tile into the running (max, sum exp(x - max), argmax)
