@@ -96,7 +96,13 @@ AttnPlan plan_attn(const zarya_slot_attn_desc* d) {
       // merge of the partials costs more than the extra workgroups save
       // (single-sequence batches: 8 splits 19.7 us, 16 splits 22.9 us)
       const int64_t base = (int64_t)d->batch * d->n_kv_heads * pl.n_rb;
-      const int64_t want = (256 + base - 1) / base;
+      int64_t want = (256 + base - 1) / base;
+      // long prefixes: two workgroups per compute unit when every split
+      // still walks at least 64 key tiles, so that one workgroup's softmax
+      // overlaps the other's MFMAs (4B shape, 256 tiles: 383 us with two
+      // splits against 424-435 us with one; at 64 tiles the extra split
+      // costs more than it overlaps)
+      if (pl.n_prefix_tiles >= 128 * want) want *= 2;
       ns = (int)std::min<int64_t>(8, std::max<int64_t>(1, want));
       ns = std::max(1, std::min(ns, pl.n_prefix_tiles / 2));
     }
