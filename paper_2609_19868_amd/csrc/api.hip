@@ -41,7 +41,7 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct AttnPlan {
   int T, G, R;
-  int n_split, tiles_per_split, n_prefix_tiles, n_rb;
+  int n_split, tiles_per_split, n_prefix_tiles, n_rb, rows_per_block;
   int64_t rows_total;
   size_t ws_bytes;
 };
@@ -83,8 +83,18 @@ AttnPlan plan_attn(const zarya_slot_attn_desc* d) {
   pl.G = d->n_q_heads / d->n_kv_heads;
   pl.R = pl.G * pl.T;
   pl.rows_total = (int64_t)d->batch * d->n_q_heads * pl.T;
-  pl.n_rb = (pl.R + kAttnRowsPerBlock - 1) / kAttnRowsPerBlock;
   pl.n_prefix_tiles = (d->prefix_len + kAttnKeysPerTile - 1) / kAttnKeysPerTile;
+  // 256-row workgroups (each K/V tile staged once for twice the rows) when
+  // they add no padding waves over 128-row ones and the prefix holds at least
+  // as many key tiles as the draft tokens (4B shape: 358 against 372-379 us;
+  // on the 4096-token training layout, all draft tokens under a causal mask,
+  // they are 6% slower)
+  const int n_narrow = (pl.R + kAttnRowsPerBlock - 1) / kAttnRowsPerBlock;
+  const int n_wide = (pl.R + kAttnWideRowsPerBlock - 1) / kAttnWideRowsPerBlock;
+  const bool wide = d->dtype == ZARYA_DTYPE_BF16 && 2 * n_wide <= n_narrow &&
+                    (int64_t)pl.n_prefix_tiles * kAttnKeysPerTile >= pl.T;
+  pl.rows_per_block = wide ? kAttnWideRowsPerBlock : kAttnRowsPerBlock;
+  pl.n_rb = wide ? n_wide : n_narrow;
   int ns = 1;
   if (d->dtype == ZARYA_DTYPE_BF16 && pl.n_prefix_tiles > 0) {
     if (d->prefix_splits > 0) {
@@ -102,7 +112,9 @@ AttnPlan plan_attn(const zarya_slot_attn_desc* d) {
       // overlaps the other's MFMAs (4B shape, 256 tiles: 383 us with two
       // splits against 424-435 us with one; at 64 tiles the extra split
       // costs more than it overlaps)
-      if (pl.n_prefix_tiles >= 128 * want) want *= 2;
+      // (256-row workgroups already hold two waves per SIMD and fit once per
+      // compute unit)
+      if (pl.rows_per_block == kAttnRowsPerBlock && pl.n_prefix_tiles >= 128 * want) want *= 2;
       ns = (int)std::min<int64_t>(8, std::max<int64_t>(1, want));
       ns = std::max(1, std::min(ns, pl.n_prefix_tiles / 2));
     }
@@ -337,6 +349,7 @@ zarya_status zarya_slot_attn(const zarya_slot_attn_desc* d, const void* q, const
   p.n_items = (int)items;
   p.per_xcd = (p.n_items + 7) / 8;
   p.rows_total = (int)pl.rows_total;
+  p.rows_per_block = pl.rows_per_block;
   return hip_status(launch_slot_attn_bf16(p, d->head_dim, stream), "slot_attn bf16 launch");
 }
 

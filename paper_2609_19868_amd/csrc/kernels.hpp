@@ -25,7 +25,8 @@ struct AttnParams {
   float scale_log2;  // softmax scale * log2(e)
   int n_split, n_rb, tiles_per_split, n_prefix_tiles;
   int per_xcd, n_items;
-  int rows_total;  // B * Hq * T
+  int rows_total;      // B * Hq * T
+  int rows_per_block;  // kAttnRowsPerBlock or kAttnWideRowsPerBlock
 };
 
 struct AttnParams32 {
@@ -154,7 +155,8 @@ int64_t mask_budget_plan(int32_t n_masked, int32_t n_steps, double alpha0, uint6
 constexpr int kAppendMaxTokens = 8192;
 
 constexpr int kAttnKeysPerTile = 64;
-constexpr int kAttnRowsPerBlock = 128;
+constexpr int kAttnRowsPerBlock = 128;      // four waves
+constexpr int kAttnWideRowsPerBlock = 256;  // eight waves: every K/V tile staged once for 256 rows
 // Tile configuration of the bf16 LM-head reduction (measured on MI355X over
 // the 0.6B/1.7B/4B shapes): 8 waves over a 256 x 256 tile, 64-deep stages,
 // three W and two hidden LDS buffers (160 KB), one workgroup per compute

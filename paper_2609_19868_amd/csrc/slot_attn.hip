@@ -7,8 +7,9 @@
 // to itself in the AR_INFILL pass), preceded by every earlier slot when
 // cross_slot = CAUSAL.
 //
-// bf16 kernel design (one workgroup = 4 waves = up to 128 query rows of one
-// GQA group, i.e. G heads x T tokens flattened; one split of the prefix keys):
+// bf16 kernel design (one workgroup = 4 or 8 waves = up to 128 or 256 query
+// rows of one GQA group, i.e. G heads x T tokens flattened; one split of the
+// prefix keys):
 //  * K/V tiles of 64 keys are staged in LDS once and shared by every query
 //    row of the group (the prefix is read from HBM once per group and split).
 //  * Scores are computed transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16:
@@ -40,8 +41,6 @@ namespace {
 
 constexpr int KT = 64;          // keys per tile
 constexpr float kRescaleLog2 = 8.f;  // growth of a row maximum (log2 units) that forces a rescale
-constexpr int NWAVE = 4;        // waves per workgroup
-constexpr int RB = NWAVE * 32;  // query rows per workgroup
 
 // XOR swizzle of the 16-byte chunk index of LDS row `kr` (D = 128: 16 chunks
 // per row; D = 64: 8).  Keeps the 32 rows of one K-fragment read and the 4
@@ -57,9 +56,11 @@ __device__ __forceinline__ int swz(int kr) {
 
 }  // namespace
 
-// NS: LDS stages (prefetch distance NS - 1 tiles).
-template <int D, int NS>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(ZARYA_ATTN_WPE))) void slot_attn_bf16_kernel(AttnParams p) {
+// NS: LDS stages (prefetch distance NS - 1 tiles).  NWAVE: waves per
+// workgroup, 32 query rows each; every wave stages its share of each K/V tile.
+template <int D, int NS, int NWAVE>
+__global__ __launch_bounds__(NWAVE * 64) __attribute__((amdgpu_waves_per_eu(ZARYA_ATTN_WPE))) void slot_attn_bf16_kernel(AttnParams p) {
+  constexpr int RB = NWAVE * 32;        // query rows per workgroup
   constexpr int ROWB = D * 2;           // bytes per key row
   constexpr int TILEB = KT * ROWB;      // bytes of one K (or V) tile
   constexpr int CPW = TILEB / 1024 / NWAVE;  // 1 KB direct loads per wave per tile (K; same for V)
@@ -135,7 +136,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(ZARYA_ATTN_
   }
 
   // ---- direct-to-LDS staging of K and V tiles: load j of a wave fills 1 KB
-  // chunk c = 4*j + wave (RPC rows); lane l lands at row RPC*c + l/LPR,
+  // chunk c = NWAVE*j + wave (RPC rows); lane l lands at row RPC*c + l/LPR,
   // physical 16-byte column l%LPR and fetches the logical column the swizzle
   // puts there.  Rows past the valid keys are clamped to the last valid row
   // (their scores are masked, so they contribute exact zeros).
@@ -496,10 +497,19 @@ __global__ __launch_bounds__(64) void slot_attn_f32_kernel(AttnParams32 p) {
 
 hipError_t launch_slot_attn_bf16(const AttnParams& p, int head_dim, hipStream_t stream) {
   const int grid = 8 * p.per_xcd;
+  const bool wide = p.rows_per_block == kAttnWideRowsPerBlock;
   if (head_dim == 128) {
-    slot_attn_bf16_kernel<128, ZARYA_ATTN_NS><<<dim3(grid), dim3(256), 0, stream>>>(p);
+    if (wide) {
+      slot_attn_bf16_kernel<128, ZARYA_ATTN_NS, 8><<<dim3(grid), dim3(512), 0, stream>>>(p);
+    } else {
+      slot_attn_bf16_kernel<128, ZARYA_ATTN_NS, 4><<<dim3(grid), dim3(256), 0, stream>>>(p);
+    }
   } else {
-    slot_attn_bf16_kernel<64, ZARYA_ATTN_NS><<<dim3(grid), dim3(256), 0, stream>>>(p);
+    if (wide) {
+      slot_attn_bf16_kernel<64, ZARYA_ATTN_NS, 8><<<dim3(grid), dim3(512), 0, stream>>>(p);
+    } else {
+      slot_attn_bf16_kernel<64, ZARYA_ATTN_NS, 4><<<dim3(grid), dim3(256), 0, stream>>>(p);
+    }
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.n_split == 1) return e;

@@ -43,7 +43,9 @@ hipError_t launch_slot_attn_bf16(const AttnParams& p, int head_dim, hipStream_t)
   CHECK(p.n_split >= 1 && p.n_split <= 64);
   CHECK((int64_t)p.tiles_per_split * p.n_split >= p.n_prefix_tiles);
   CHECK(p.n_split == 1 || (int64_t)p.tiles_per_split * (p.n_split - 1) < p.n_prefix_tiles);
-  CHECK((int64_t)p.n_rb * kAttnRowsPerBlock >= p.R && p.R == p.G * p.T);
+  CHECK(p.rows_per_block == kAttnRowsPerBlock || p.rows_per_block == kAttnWideRowsPerBlock);
+  CHECK((int64_t)p.n_rb * p.rows_per_block >= p.R && (int64_t)(p.n_rb - 1) * p.rows_per_block < p.R &&
+        p.R == p.G * p.T);
   CHECK(p.n_items == p.B * p.Hkv * p.n_split * p.n_rb);
   CHECK(p.per_xcd * 8 >= p.n_items && (p.per_xcd - 1) * 8 < p.n_items);
   if (p.n_split > 1) {

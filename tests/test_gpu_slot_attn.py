@@ -58,6 +58,11 @@ SMALL_BF16 = [
     # one key past a tile, and slots longer than several key tiles
     ("p65_long_slots", dict(batch=1, n_q_heads=2, n_kv_heads=1, prefix_len=65, n_slots=2, slot_len=200)),
     ("p1", dict(batch=3, n_q_heads=2, n_kv_heads=2, prefix_len=1, n_slots=3, slot_len=4)),
+    # 256-row (eight-wave) workgroups: two of them, the second with 112 padding rows; D = 64;
+    # and 260 rows, which stay on three 128-row workgroups
+    ("wide_two_blocks", dict(batch=2, n_q_heads=8, n_kv_heads=2, prefix_len=333, n_slots=10, slot_len=10)),
+    ("d64_wide", dict(batch=1, n_q_heads=8, n_kv_heads=2, head_dim=64, prefix_len=300, n_slots=8, slot_len=8)),
+    ("g2_three_row_blocks", dict(batch=1, n_q_heads=4, n_kv_heads=2, prefix_len=190, n_slots=10, slot_len=13)),
 ]
 
 
@@ -87,9 +92,10 @@ def test_bf16_per_slot_pass_and_cross_causal():
         check_attn(to_f64(out), to_f64(lse), O, L, "bf16", f"slot_pass cross={cross}")
 
 
-def test_bf16_split_counts_agree_and_runs_are_bitwise_identical():
+@pytest.mark.parametrize("over", [dict(), dict(n_q_heads=8, n_kv_heads=2)], ids=["rows128", "rows256_wide"])
+def test_bf16_split_counts_agree_and_runs_are_bitwise_identical(over):
     dev = require_gpu()
-    wl = W.WORKLOADS["qwen0.6b"].replace(batch=2, prefix_len=1000, hidden=0, vocab=0, seed=79)
+    wl = W.WORKLOADS["qwen0.6b"].replace(batch=2, prefix_len=1000, hidden=0, vocab=0, seed=79, **over)
     xd, xf = attn_inputs_dev(wl, dev)
     O, L = _oracle(xf, wl, oracle.PASS_DIFFUSION)
     outs = {}
@@ -117,6 +123,7 @@ RAGGED = [
     ("bf16_d64", "bf16", dict(batch=3, n_q_heads=4, n_kv_heads=2, head_dim=64, prefix_len=257, n_slots=4,
                               slot_len=6)),
     ("f32", "f32", dict(batch=3, n_q_heads=2, n_kv_heads=1, head_dim=64, prefix_len=70, n_slots=3, slot_len=4)),
+    ("bf16_wide", "bf16", dict(batch=3, n_q_heads=8, n_kv_heads=2, prefix_len=300, n_slots=8, slot_len=8)),
 ]
 
 
