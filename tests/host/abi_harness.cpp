@@ -37,9 +37,11 @@ static bool in_ws(const void* p, size_t bytes) {
 static int g_launches = 0;
 
 namespace zarya {
+static AttnParams g_last_attn;  // the parameters of the last bf16 attention launch
 
 hipError_t launch_slot_attn_bf16(const AttnParams& p, int head_dim, hipStream_t) {
   ++g_launches;
+  g_last_attn = p;
   CHECK(p.n_split >= 1 && p.n_split <= 64);
   CHECK((int64_t)p.tiles_per_split * p.n_split >= p.n_prefix_tiles);
   CHECK(p.n_split == 1 || (int64_t)p.tiles_per_split * (p.n_split - 1) < p.n_prefix_tiles);
@@ -161,6 +163,61 @@ static void attn_cases(std::mt19937_64& rng) {
   }
 }
 
+// The work decomposition the planner picks for the named workloads (rows per
+// workgroup, row blocks, prefix splits): 256-row blocks only where they add no
+// padding and the prefix dominates, two splits per group where that reaches
+// about one workgroup per compute unit, and a doubling for 128-row blocks on
+// long prefixes.
+static void named_plans() {
+  struct Case {
+    const char* name;
+    int B, Hq, Hkv, P, S, L, cross;
+    int rows_per_block, n_rb, n_split;
+  };
+  const Case cases[] = {
+      {"qwen0.6b", 16, 16, 8, 2048, 8, 8, 0, 128, 1, 2},
+      {"qwen1.7b", 32, 16, 8, 4096, 16, 4, 0, 128, 1, 1},
+      {"qwen4b", 8, 32, 8, 16384, 8, 16, 0, 256, 2, 2},
+      {"qwen4b with 17-token slots: 128-row blocks pad less", 8, 32, 8, 16384, 8, 17, 0, 128, 5, 2},
+      {"qwen0.6b batch 1", 1, 16, 8, 2048, 8, 8, 0, 128, 1, 8},
+      {"layout", 8, 16, 8, 0, 128, 32, 1, 128, 64, 1},
+      {"modeA", 16, 16, 8, 2048, 260, 1, 1, 128, 5, 1},
+      {"128-row blocks, 256 prefix tiles: two splits doubled", 16, 16, 8, 16384, 8, 8, 0, 128, 1, 4},
+      {"128-row blocks, 128 prefix tiles: two splits kept", 16, 16, 8, 8192, 8, 8, 0, 128, 1, 2},
+  };
+  for (const Case& c : cases) {
+    zarya_slot_attn_desc d{};
+    d.batch = c.B;
+    d.n_q_heads = c.Hq;
+    d.n_kv_heads = c.Hkv;
+    d.head_dim = 128;
+    d.prefix_len = c.P;
+    d.kv_capacity = c.P;
+    d.n_slots = c.S;
+    d.slot_len = c.L;
+    d.softmax_scale = 0.088f;
+    d.pass = 0;
+    d.cross_slot = c.cross;
+    d.dtype = ZARYA_DTYPE_BF16;
+    size_t ws = 0;
+    CHECK(zarya_slot_attn_workspace_size(&d, &ws) == ZARYA_OK);
+    g_ws_lo = 0x100000000ull;
+    g_ws_hi = g_ws_lo + ws;
+    void* p = fake(0x200000000ull);
+    const int before = g_launches;
+    expect_launch(zarya_slot_attn(&d, p, p, p, p, p, nullptr, nullptr, p, nullptr, ws ? fake(g_ws_lo) : nullptr, ws,
+                                  nullptr),
+                  before, c.name);
+    const zarya::AttnParams& a = zarya::g_last_attn;
+    if (a.rows_per_block != c.rows_per_block || a.n_rb != c.n_rb || a.n_split != c.n_split) {
+      std::printf("FAIL plan %s: rows/block %d, row blocks %d, splits %d (expected %d, %d, %d)\n", c.name,
+                  a.rows_per_block, a.n_rb, a.n_split, c.rows_per_block, c.n_rb, c.n_split);
+      ++g_fail;
+    }
+    ++g_checks;
+  }
+}
+
 static void conf_cases(std::mt19937_64& rng) {
   for (int it = 0; it < 400; ++it) {
     zarya_conf_desc d{};
@@ -249,6 +306,7 @@ static void budget_cases(std::mt19937_64& rng) {
 int main() {
   std::mt19937_64 rng(20260);
   attn_cases(rng);
+  named_plans();
   conf_cases(rng);
   small_call_cases();
   budget_cases(rng);
