@@ -63,6 +63,7 @@ APPEND_CASES = [
     ("bf16_d64", "bf16", 3, 2, 64, 90, 4, 16),
     ("f32_d64", "f32", 4, 3, 64, 50, 5, 3),
     ("bf16_long_slots", "bf16", 2, 1, 128, 5000, 8, 512),
+    ("bf16_max_tokens", "bf16", 3, 1, 64, 9000, 1024, 8),  # S*L = 8192 draft tokens, the largest accepted
 ]
 
 
