@@ -99,7 +99,7 @@ def test_bf16_split_counts_agree_and_runs_are_bitwise_identical(over):
     xd, xf = attn_inputs_dev(wl, dev)
     O, L = _oracle(xf, wl, oracle.PASS_DIFFUSION)
     outs = {}
-    for splits in (1, 2, 4, 8):
+    for splits in (1, 2, 4, 8, 16):  # 16 (one key tile each): the merge's path past its first 8 splits
         say(f"slot_attn bf16 splits={splits}")
         out, lse = _run(xd, wl, Z.PASS_DIFFUSION, splits=splits)
         check_attn(to_f64(out), to_f64(lse), O, L, "bf16", f"splits={splits}")
@@ -107,7 +107,7 @@ def test_bf16_split_counts_agree_and_runs_are_bitwise_identical(over):
         assert torch.equal(out.view(torch.int16), out2.view(torch.int16)), "rerun differs"
         assert torch.equal(lse, lse2), "rerun LSE differs"
         outs[splits] = (to_f64(out), to_f64(lse))
-    for splits in (2, 4, 8):
+    for splits in (2, 4, 8, 16):
         # each split rounds its probabilities to bf16 against its own running
         # maximum, so splits agree to that rounding (2^-9 relative per term of a
         # convex combination of |v| <= ~5), not bit for bit; LSE is float32 only
