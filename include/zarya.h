@@ -287,7 +287,8 @@ typedef struct zarya_kv_append_desc {
  * prefix_lens      [B] int32 in/out
  * k_cache, v_cache [B, Hkv, C, D] dtype in/out
  * A row whose prefix_lens[b] is negative or whose append would pass C is left
- * unchanged, its length included (checked on the GPU).
+ * unchanged, its length included (checked on the GPU).  The slot K/V must not
+ * overlap the caches (the copies read and write them concurrently).
  */
 zarya_status zarya_kv_append(const zarya_kv_append_desc* desc, const void* k_slot, const void* v_slot,
                              const uint8_t* accepted, const int32_t* order, int32_t* prefix_lens,
