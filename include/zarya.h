@@ -174,7 +174,7 @@ zarya_status zarya_slot_attn(const zarya_slot_attn_desc* desc, const void* q, co
  */
 typedef struct zarya_conf_desc {
   int32_t n_rows; /* M >= 1                                              */
-  int32_t hidden; /* H >= 1; a multiple of 8 for BF16                    */
+  int32_t hidden; /* H >= 1; for BF16 a multiple of 8 and <= 4194304      */
   int32_t vocab;  /* V >= 1                                              */
   int32_t dtype;  /* zarya_dtype of hidden and w_vocab                   */
 } zarya_conf_desc;

@@ -147,6 +147,9 @@ zarya_status check_conf_desc(const zarya_conf_desc* d) {
     return fail(ZARYA_ERR_INVALID_ARGUMENT, "unknown dtype %d", d->dtype);
   if (d->dtype == ZARYA_DTYPE_BF16 && d->hidden % 8 != 0)
     return fail(ZARYA_ERR_UNSUPPORTED, "bf16 hidden size %d is not a multiple of 8", d->hidden);
+  // a 256-row W tile is addressed with 32-bit byte offsets
+  if (d->dtype == ZARYA_DTYPE_BF16 && d->hidden > 4194304)
+    return fail(ZARYA_ERR_UNSUPPORTED, "bf16 hidden size %d exceeds 4194304", d->hidden);
   if (d->dtype == ZARYA_DTYPE_F32 && d->hidden > 8192)
     return fail(ZARYA_ERR_UNSUPPORTED, "f32 hidden size %d exceeds 8192", d->hidden);
   if (d->dtype == ZARYA_DTYPE_F32 && d->n_rows > 65535)

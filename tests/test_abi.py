@@ -114,6 +114,7 @@ def _conf_status(desc, ptr=1, ws_bytes=1 << 40):
     (dict(dtype=3), _lib.ERR_INVALID_ARGUMENT),
     (dict(hidden=1001), _lib.ERR_UNSUPPORTED),
     (dict(dtype=0, hidden=10000), _lib.ERR_UNSUPPORTED),
+    (dict(hidden=4194304 + 8), _lib.ERR_UNSUPPORTED),  # 256-row W tiles need 32-bit offsets
 ])
 def test_slot_confidence_rejects_bad_descriptors(bad, code):
     base = dict(n_rows=64, hidden=1024, vocab=151936, dtype=1)
