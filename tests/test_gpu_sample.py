@@ -159,7 +159,7 @@ def test_draws_follow_the_tempered_softmax():
     assert np.allclose(sp, np.exp(zs - lse), rtol=1e-3)
 
 
-@pytest.mark.parametrize("name", ["qwen0.6b", "qwen4b"])
+@pytest.mark.parametrize("name", ["qwen0.6b", "qwen1.7b", "qwen4b"])
 def test_full_size_sampled(name):
     """Full vocabulary and row count in the benchmark's launch configuration;
     the oracle checks a sample of rows (every vocab entry of each)."""
