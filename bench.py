@@ -377,15 +377,19 @@ def verification_step(dev, wl, s, conf_out, sel_out, K):
         plens.copy_(plens0)
         one()
     torch.cuda.synchronize()
-    per = []
+    # steps run back to back (the reset is a copy on the same stream, between
+    # the timed events); the host reads the events and counts once at the end
+    ev_steps = []
     appended = []
     for _ in range(K):
         plens.copy_(plens0)
         evs = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
         one(evs)
-        torch.cuda.synchronize()
-        per.append([evs[j].elapsed_time(evs[j + 1]) * 1e3 for j in range(4)])
-        appended.append(float((plens - plens0).float().mean()))
+        ev_steps.append(evs)
+        appended.append((plens - plens0).float().mean())
+    torch.cuda.synchronize()
+    per = [[evs[j].elapsed_time(evs[j + 1]) * 1e3 for j in range(4)] for evs in ev_steps]
+    appended = [float(a) for a in appended]
     m = [statistics.mean(p[j] for p in per) for j in range(4)]
     return {"slot_attn_ar_infill_us": m[0], "slot_confidence_targets_us": m[1], "verify_accept_us": m[2],
             "kv_append_us": m[3], "step_us": sum(m), "steps_per_s": 1e6 / sum(m),
@@ -510,14 +514,15 @@ def mode_a_step(dev, w_vocab, K):
             mask.copy_(mask0)
             one(i, rule)
         torch.cuda.synchronize()
-        per = []
-        for i in range(K):
+        ev_steps = []
+        for i in range(K):  # back to back; the resets run between the timed events
             plens.copy_(plens0)
             mask.copy_(mask0)
             evs = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
             one(100 + i, rule, evs)
-            torch.cuda.synchronize()
-            per.append([evs[j].elapsed_time(evs[j + 1]) * 1e3 for j in range(4)])
+            ev_steps.append(evs)
+        torch.cuda.synchronize()
+        per = [[evs[j].elapsed_time(evs[j + 1]) * 1e3 for j in range(4)] for evs in ev_steps]
         m = [statistics.mean(p[j] for p in per) for j in range(4)]
         if rule == Z.REVEAL_CONFIDENCE:
             parts = {"slot_attn_causal_us": m[0], "slot_sample_all_masked_us": m[1], "mdm_reveal_us": m[2]}
