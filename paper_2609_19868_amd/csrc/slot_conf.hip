@@ -586,10 +586,20 @@ __global__ __launch_bounds__(256) void slot_conf_f32_kernel(ConfParams p) {
 // product spread over the 64 lanes of a wave (every lane gets the sum).
 __device__ float row_logit(const ConfMergeParams& p, int hrow, int v, int lane) {
   float z = 0.f;
-  if (p.bf16) {
+  if (p.bf16) {  // 16-byte loads (H is a multiple of 8): one or two load rounds for H <= 1024
     const uint16_t* hr = static_cast<const uint16_t*>(p.hidden) + (size_t)hrow * p.H;
     const uint16_t* wr = static_cast<const uint16_t*>(p.w_vocab) + (size_t)v * p.H;
-    for (int k = lane; k < p.H; k += 64) z = fmaf(bf16_to_f32(hr[k]), bf16_to_f32(wr[k]), z);
+#pragma unroll 4
+    for (int k = lane * 8; k < p.H; k += 512) {
+      const uint4 hv = *reinterpret_cast<const uint4*>(hr + k);
+      const uint4 wv = *reinterpret_cast<const uint4*>(wr + k);
+      const uint32_t hw[4] = {hv.x, hv.y, hv.z, hv.w}, ww[4] = {wv.x, wv.y, wv.z, wv.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        z = fmaf(__uint_as_float(hw[e] << 16), __uint_as_float(ww[e] << 16), z);
+        z = fmaf(__uint_as_float(hw[e] & 0xffff0000u), __uint_as_float(ww[e] & 0xffff0000u), z);
+      }
+    }
   } else {
     const float* hr = static_cast<const float*>(p.hidden) + (size_t)hrow * p.H;
     const float* wr = static_cast<const float*>(p.w_vocab) + (size_t)v * p.H;
