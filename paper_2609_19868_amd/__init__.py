@@ -78,8 +78,10 @@ def _ptr(t):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 
 
-def _stream():
-    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+def _stream(dev):
+    """The current stream of `dev` (calls run inside `torch.cuda.device(dev)`,
+    so that the library launches on the tensors' device)."""
+    return ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
 
 
 def _need(t, name, shape, dtype, device):
@@ -142,10 +144,11 @@ def slot_attn(q, k_cache, v_cache, k_slot, v_slot, n_slots, slot_len, pass_=PASS
     ws_bytes = _lib.slot_attn_workspace_size(desc)
     if workspace is None and ws_bytes > 0:
         workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
-    _lib.check(_lib.lib().zarya_slot_attn(
-        ctypes.byref(desc), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(k_slot), _ptr(v_slot), _ptr(slot_pass),
-        _ptr(prefix_lens), _ptr(out), _ptr(lse), _ptr(workspace), 0 if workspace is None else workspace.numel(),
-        _stream()))
+    with torch.cuda.device(dev):  # the library launches on the current device
+        _lib.check(_lib.lib().zarya_slot_attn(
+            ctypes.byref(desc), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(k_slot), _ptr(v_slot), _ptr(slot_pass),
+            _ptr(prefix_lens), _ptr(out), _ptr(lse), _ptr(workspace), 0 if workspace is None else workspace.numel(),
+            _stream(dev)))
     return out, lse
 
 
@@ -175,10 +178,11 @@ def slot_confidence(hidden, w_vocab, target_ids=None, out=None, workspace=None):
     ws_bytes = _lib.slot_confidence_workspace_size(desc)
     if workspace is None:
         workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
-    _lib.check(_lib.lib().zarya_slot_confidence(
-        ctypes.byref(desc), _ptr(hidden), _ptr(w_vocab), _ptr(target_ids), _ptr(out["max_prob"]),
-        _ptr(out["argmax"]), _ptr(out.get("lse")), _ptr(out.get("target_prob")), _ptr(workspace),
-        workspace.numel(), _stream()))
+    with torch.cuda.device(dev):  # the library launches on the current device
+        _lib.check(_lib.lib().zarya_slot_confidence(
+            ctypes.byref(desc), _ptr(hidden), _ptr(w_vocab), _ptr(target_ids), _ptr(out["max_prob"]),
+            _ptr(out["argmax"]), _ptr(out.get("lse")), _ptr(out.get("target_prob")), _ptr(workspace),
+            workspace.numel(), _stream(dev)))
     return out
 
 
@@ -210,10 +214,11 @@ def slot_sample(hidden, w_vocab, temperature, seed, offset=0, rows=None, out=Non
     ws_bytes = _lib.slot_sample_workspace_size(desc)
     if workspace is None:
         workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
-    _lib.check(_lib.lib().zarya_slot_sample(
-        ctypes.byref(desc), ctypes.byref(params), _ptr(hidden), _ptr(rows), N, _ptr(w_vocab), _ptr(out["sample_id"]),
-        _ptr(out["sample_prob"]), _ptr(out.get("max_prob")), _ptr(out.get("lse")), _ptr(workspace),
-        workspace.numel(), _stream()))
+    with torch.cuda.device(dev):  # the library launches on the current device
+        _lib.check(_lib.lib().zarya_slot_sample(
+            ctypes.byref(desc), ctypes.byref(params), _ptr(hidden), _ptr(rows), N, _ptr(w_vocab), _ptr(out["sample_id"]),
+            _ptr(out["sample_prob"]), _ptr(out.get("max_prob")), _ptr(out.get("lse")), _ptr(workspace),
+            workspace.numel(), _stream(dev)))
     return out
 
 
@@ -250,9 +255,10 @@ def mdm_reveal(mask, k, rule=REVEAL_CONFIDENCE, conf=None, seed=0, offset=0, sam
     if out is None:
         out = (torch.empty((B, N), dtype=torch.int32, device=dev), torch.empty((B,), dtype=torch.int32, device=dev))
     order, n = out
-    _lib.check(_lib.lib().zarya_mdm_reveal(
-        B, N, _ptr(conf), _ptr(mask), _ptr(k), int(rule), int(seed) & (2**64 - 1), int(offset) & (2**64 - 1),
-        _ptr(sample_id), _ptr(tokens), _ptr(order), _ptr(n), _stream()))
+    with torch.cuda.device(dev):  # the library launches on the current device
+        _lib.check(_lib.lib().zarya_mdm_reveal(
+            B, N, _ptr(conf), _ptr(mask), _ptr(k), int(rule), int(seed) & (2**64 - 1), int(offset) & (2**64 - 1),
+            _ptr(sample_id), _ptr(tokens), _ptr(order), _ptr(n), _stream(dev)))
     return order, n
 
 
@@ -274,9 +280,10 @@ def select_slots(token_conf, slot_open=None, conf_rule=SLOT_CONF_FIRST_TOKEN, ru
             torch.empty((B,), dtype=torch.int32, device=dev),
         )
     slot_conf, selected, n_selected = out
-    _lib.check(_lib.lib().zarya_select_slots(
-        B, S, L, _ptr(token_conf), _ptr(slot_open), int(conf_rule), int(rule), float(threshold), int(k),
-        _ptr(slot_conf), _ptr(selected), _ptr(n_selected), _stream()))
+    with torch.cuda.device(dev):  # the library launches on the current device
+        _lib.check(_lib.lib().zarya_select_slots(
+            B, S, L, _ptr(token_conf), _ptr(slot_open), int(conf_rule), int(rule), float(threshold), int(k),
+            _ptr(slot_conf), _ptr(selected), _ptr(n_selected), _stream(dev)))
     return slot_conf, selected, n_selected
 
 
@@ -299,9 +306,10 @@ def verify_accept(token_prob, selected, token_threshold=0.4, rule=ACCEPT_PREFIX,
             torch.empty((B,), dtype=torch.int32, device=dev),
         )
     accepted, n_accepted, n_total = out
-    _lib.check(_lib.lib().zarya_verify_accept(
-        B, S, L, _ptr(token_prob), _ptr(selected), float(token_threshold), int(rule), _ptr(accepted),
-        _ptr(n_accepted), _ptr(n_total), _stream()))
+    with torch.cuda.device(dev):  # the library launches on the current device
+        _lib.check(_lib.lib().zarya_verify_accept(
+            B, S, L, _ptr(token_prob), _ptr(selected), float(token_threshold), int(rule), _ptr(accepted),
+            _ptr(n_accepted), _ptr(n_total), _stream(dev)))
     return accepted, n_accepted, n_total
 
 
@@ -324,7 +332,8 @@ def kv_append(k_cache, v_cache, prefix_lens, k_slot, v_slot, accepted, order):
     _need(prefix_lens, "prefix_lens", (B,), torch.int32, dev)
     desc = _lib.KvAppendDesc(batch=B, n_kv_heads=Hkv, head_dim=D, kv_capacity=C, n_slots=S, slot_len=L,
                              dtype=_DT[dt])
-    _lib.check(_lib.lib().zarya_kv_append(
-        ctypes.byref(desc), _ptr(k_slot), _ptr(v_slot), _ptr(accepted), _ptr(order), _ptr(prefix_lens),
-        _ptr(k_cache), _ptr(v_cache), _stream()))
+    with torch.cuda.device(dev):  # the library launches on the current device
+        _lib.check(_lib.lib().zarya_kv_append(
+            ctypes.byref(desc), _ptr(k_slot), _ptr(v_slot), _ptr(accepted), _ptr(order), _ptr(prefix_lens),
+            _ptr(k_cache), _ptr(v_cache), _stream(dev)))
     return k_cache, v_cache, prefix_lens
