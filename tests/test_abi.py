@@ -248,3 +248,17 @@ def test_library_has_no_undefined_own_symbols():
     out = subprocess.run(["nm", "-D", "--undefined-only", _lib.LIB_PATH], capture_output=True, text=True,
                          check=True).stdout
     assert "zarya" not in out, out
+
+
+def test_binding_refuses_host_tensors():
+    """Host (CPU) tensors never reach the library: the binding runs each call
+    with the tensors' GPU current, and a CPU device is refused."""
+    import torch
+    import paper_2609_19868_amd as Z
+
+    h = torch.zeros(4, 64, dtype=torch.bfloat16)
+    w = torch.zeros(100, 64, dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="cuda"):
+        Z.slot_confidence(h, w)
+    with pytest.raises(ValueError, match="cuda"):
+        Z.select_slots(torch.zeros(2, 3, 4))
