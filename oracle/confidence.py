@@ -13,7 +13,9 @@ Paper passages this follows:
 
 Readings where the paper is silent: the probability is taken at temperature 1
 with no sampling noise; the argmax takes the lowest vocabulary id among equal
-maxima.
+maxima.  A row whose logits include a NaN or an infinity (a NaN or infinite
+hidden value, say) has no softmax: its log-sum-exp is not finite, and such a
+row reports argmax -1 and NaN for every probability and the log-sum-exp.
 
 For each row of ``hidden`` the oracle returns the max logit, its id, the
 log-sum-exp of the row, the largest softmax probability ``exp(m - lse)``, the
@@ -52,22 +54,24 @@ def slot_confidence(hidden, w_vocab, target_ids=None, row_chunk=256):
         out["target_prob"] = np.empty(M)
     for r0 in range(0, M, row_chunk):
         r1 = min(M, r0 + row_chunk)
-        logits = np.asarray(h[r0:r1], dtype=np.float64) @ w.T
-        idx = np.argmax(logits, axis=1)  # first occurrence: lowest id on ties
-        m = logits[np.arange(r1 - r0), idx]
-        lse = m + np.log(np.exp(logits - m[:, None]).sum(axis=1))
-        out["argmax"][r0:r1] = idx
-        out["max_logit"][r0:r1] = m
-        out["lse"][r0:r1] = lse
-        out["max_prob"][r0:r1] = np.exp(m - lse)
-        if logits.shape[1] > 1:
-            second = np.partition(logits, -2, axis=1)[:, -2]
-            out["top2_gap"][r0:r1] = m - second
-        else:
-            out["top2_gap"][r0:r1] = np.inf
-        if target_ids is not None:
-            t = target_ids[r0:r1]
-            out["target_prob"][r0:r1] = np.exp(logits[np.arange(r1 - r0), t] - lse)
+        with np.errstate(invalid="ignore", over="ignore"):
+            logits = np.asarray(h[r0:r1], dtype=np.float64) @ w.T
+            idx = np.argmax(logits, axis=1)  # first occurrence: lowest id on ties
+            m = logits[np.arange(r1 - r0), idx]
+            lse = m + np.log(np.exp(logits - m[:, None]).sum(axis=1))
+            bad = ~np.isfinite(lse)  # a NaN or infinite logit: no softmax
+            out["argmax"][r0:r1] = np.where(bad, -1, idx)
+            out["max_logit"][r0:r1] = np.where(bad, np.nan, m)
+            out["lse"][r0:r1] = np.where(bad, np.nan, lse)
+            out["max_prob"][r0:r1] = np.where(bad, np.nan, np.exp(m - lse))
+            if logits.shape[1] > 1:
+                second = np.partition(logits, -2, axis=1)[:, -2]
+                out["top2_gap"][r0:r1] = np.where(bad, np.inf, m - second)
+            else:
+                out["top2_gap"][r0:r1] = np.inf
+            if target_ids is not None:
+                t = target_ids[r0:r1]
+                out["target_prob"][r0:r1] = np.where(bad, np.nan, np.exp(logits[np.arange(r1 - r0), t] - lse))
     return out
 
 
@@ -86,6 +90,8 @@ def slot_confidence_loops(hidden, w_vocab, target_ids=None):
             if logits[v] > best:
                 best, best_id = logits[v], v
         lse = best + math.log(math.fsum(math.exp(x - best) for x in logits))
+        if not math.isfinite(lse):  # a NaN or infinite logit: no softmax
+            lse, best_id = math.nan, -1
         res["max_prob"].append(math.exp(best - lse))
         res["argmax"].append(best_id)
         res["lse"].append(lse)

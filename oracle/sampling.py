@@ -25,6 +25,9 @@ Readings where the paper is silent (each listed in the design notes): the
 counter layout above; the reported probability of the drafted token is its
 model probability softmax(z)[x] (temperature 1), the same quantity the greedy
 path reports as max_prob; ties of the perturbed scores go to the lowest id.
+A row whose logits include a NaN or an infinity has no distribution to draw
+from (its log-sum-exp is not finite): it reports sample id -1 and NaN
+probabilities, as the greedy confidence does.
 """
 
 from __future__ import annotations
@@ -96,22 +99,24 @@ def slot_sample(hidden, w_vocab, temperature, seed, offset, row_chunk=256, row_i
     out["sample_id"] = np.empty(M, dtype=np.int64)
     for r0 in range(0, M, row_chunk):
         r1 = min(M, r0 + row_chunk)
-        z = h[r0:r1] @ w.T
-        u = uniforms(ids[r0:r1], V, seed, offset)
-        score = z / T + gumbel(u)
-        idx = np.argmax(score, axis=1)  # first (lowest) id on ties
-        m = z.max(axis=1)
-        lse = m + np.log(np.exp(z - m[:, None]).sum(axis=1))
-        zx = z[np.arange(r1 - r0), idx]
-        if V > 1:
-            top2 = np.sort(score, axis=1)[:, -2:]
-            gap = top2[:, 1] - top2[:, 0]
-        else:
-            gap = np.full(r1 - r0, np.inf)
-        out["sample_id"][r0:r1] = idx
-        out["best_score"][r0:r1] = score[np.arange(r1 - r0), idx]
-        out["sample_logit"][r0:r1] = zx
-        out["lse"][r0:r1] = lse
-        out["sample_prob"][r0:r1] = np.exp(zx - lse)
-        out["score_gap"][r0:r1] = gap
+        with np.errstate(invalid="ignore", over="ignore"):
+            z = h[r0:r1] @ w.T
+            u = uniforms(ids[r0:r1], V, seed, offset)
+            score = z / T + gumbel(u)
+            idx = np.argmax(score, axis=1)  # first (lowest) id on ties
+            m = z.max(axis=1)
+            lse = m + np.log(np.exp(z - m[:, None]).sum(axis=1))
+            bad = ~np.isfinite(lse)  # a NaN or infinite logit: no distribution to draw from
+            zx = z[np.arange(r1 - r0), idx]
+            if V > 1:
+                top2 = np.sort(score, axis=1)[:, -2:]
+                gap = np.where(bad, np.inf, top2[:, 1] - top2[:, 0])
+            else:
+                gap = np.full(r1 - r0, np.inf)
+            out["sample_id"][r0:r1] = np.where(bad, -1, idx)
+            out["best_score"][r0:r1] = np.where(bad, np.nan, score[np.arange(r1 - r0), idx])
+            out["sample_logit"][r0:r1] = np.where(bad, np.nan, zx)
+            out["lse"][r0:r1] = np.where(bad, np.nan, lse)
+            out["sample_prob"][r0:r1] = np.where(bad, np.nan, np.exp(zx - lse))
+            out["score_gap"][r0:r1] = gap
     return out

@@ -16,7 +16,9 @@ Paper passages this follows:
 Readings where the paper is silent: "exceeding" is a strict comparison; the
 fallback takes the lowest slot index among equally confident slots; the
 output lists the chosen slots in first-hitting order, i.e. by descending
-confidence with ties going to the lower slot index.
+confidence with ties going to the lower slot index.  A NaN slot confidence
+(for instance from a NaN token probability) counts as -inf: it ranks after
+every other open slot, never exceeds the threshold, and is reported as -inf.
 
 Precision: the selection is an integer decision taken from floating point, so
 this oracle takes it in the precision of the kernel it checks: slot
@@ -60,6 +62,7 @@ def select_slots(token_conf, slot_open=None, conf_rule=CONF_FIRST_TOKEN, rule=SE
     n_selected [B] int32).
     """
     conf = slot_conf(token_conf, conf_rule)
+    conf = np.where(np.isnan(conf), np.float32(-np.inf), conf).astype(np.float32)  # NaN ranks as -inf
     B, S = conf.shape
     is_open = np.ones((B, S), dtype=bool) if slot_open is None else (np.asarray(slot_open) != 0)
     tau = np.float32(threshold)

@@ -29,7 +29,8 @@ Readings where the paper is silent (each listed in the design notes):
 * Accepted tokens are appended slot by slot in the given order (the selection
   order), positions inside a slot in order.  Attention over the cache does not
   depend on the order of the keys, so any fixed order works; this one keeps a
-  slot's tokens contiguous.
+  slot's tokens contiguous.  A slot listed again in the order is skipped: the
+  cache grows by the accepted tokens, each committed once.
 """
 
 from __future__ import annotations
@@ -84,7 +85,8 @@ def kv_append(k_cache, v_cache, prefix_lens, k_slot, v_slot, accepted, order):
     k_slot, v_slot   [B, Hkv, T, D]   the draft tokens' own K/V, T = S*L
     accepted         [B, S, L]        1 = accepted
     order            [B, S]           slots in append order; the first -1 ends it,
-                                      ids past S are skipped
+                                      ids past S are skipped, and a slot listed
+                                      again is skipped (its tokens are committed once)
 
     A batch row whose appended length would exceed the capacity C is left
     unchanged.  Returns (k_cache', v_cache', prefix_lens').
@@ -99,12 +101,14 @@ def kv_append(k_cache, v_cache, prefix_lens, k_slot, v_slot, accepted, order):
     ordr = np.asarray(order).reshape(B, S)
     for b in range(B):
         tokens = []
+        listed = set()
         for i in range(S):
             s = int(ordr[b, i])
             if s < 0:
                 break
-            if s >= S:
-                continue
+            if s >= S or s in listed:
+                continue  # not a slot id, or a slot already appended
+            listed.add(s)
             tokens += [s * L + r for r in range(L) if acc[b, s, r]]
         p0 = int(plens[b])
         if p0 < 0 or p0 + len(tokens) > C:

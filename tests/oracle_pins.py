@@ -372,6 +372,32 @@ def check_conf_ties(conf):
     assert r["top2_gap"][0] == 0.0
 
 
+def check_conf_nonfinite_rows(conf):
+    """Rows with a NaN or infinite hidden value: IEEE arithmetic makes some of
+    their logits NaN or infinite, scipy's logsumexp of such a row is not
+    finite, and the row reports argmax -1 and NaN probabilities (the rule the
+    header states).  Every other row keeps the values it has without them."""
+    rng = np.random.default_rng(27)
+    V, H, M = 300, 16, 6
+    w = 0.3 * rng.standard_normal((V, H))
+    h = rng.standard_normal((M, H))
+    t = rng.integers(0, V, M)
+    clean = conf(h, w, target_ids=t)
+    h2 = h.copy()
+    h2[1, 3] = np.nan
+    h2[4, 0] = np.inf
+    with np.errstate(invalid="ignore", over="ignore"):
+        lse_scipy = scipy.special.logsumexp(h2 @ w.T, axis=1)
+    bad = ~np.isfinite(lse_scipy)
+    assert bad.tolist() == [False, True, False, False, True, False], bad
+    r = conf(h2, w, target_ids=t)
+    assert np.all(r["argmax"][bad] == -1), r["argmax"]
+    for key in ("max_prob", "lse", "target_prob"):
+        assert np.all(np.isnan(r[key][bad])), (key, r[key])
+        assert np.array_equal(r[key][~bad], clean[key][~bad]), key
+    assert np.array_equal(r["argmax"][~bad], clean["argmax"][~bad])
+
+
 CONFIDENCE_CHECKS = [
     check_conf_library,
     check_conf_bruteforce,
@@ -379,6 +405,7 @@ CONFIDENCE_CHECKS = [
     check_conf_planted,
     check_conf_sums_to_one,
     check_conf_ties,
+    check_conf_nonfinite_rows,
 ]
 
 
@@ -401,7 +428,34 @@ def check_select_golden(select):
         assert np.all(sel[0, n[0]:] == -1), f"{case['name']}: padding"
 
 
-SELECTION_CHECKS = [check_select_golden]
+def check_select_nan_reported(select):
+    """A NaN slot confidence is reported as -inf and selects like -inf, for
+    both confidence rules; closed slots still report -1."""
+    rng = np.random.default_rng(31)
+    B, S, L = 3, 7, 3
+    tc = rng.random((B, S, L)).astype(np.float32)
+    tc[0, 2, 0] = np.nan  # first token NaN: the slot's confidence under both rules
+    tc[1, 4, 1] = np.nan  # a later token NaN: only the mean is NaN
+    tc[2, :, 0] = np.nan
+    op = np.ones((B, S), dtype=np.uint8)
+    op[2, 5] = 0
+    for cr in (0, 1):
+        minus = tc.copy()
+        minus[np.isnan(minus)] = -np.inf
+        for rule, k in ((0, 1), (1, 4), (1, S)):
+            sc, sel, n = select(tc, op, cr, rule, 0.5, k)
+            sc2, sel2, n2 = select(minus, op, cr, rule, 0.5, k)
+            assert np.array_equal(sel, sel2) and np.array_equal(n, n2), (cr, rule, k)
+            assert np.array_equal(sc, sc2), (cr, rule, k)
+            assert not np.isnan(sc).any()
+            assert sc[2, 5] == -1.0
+    sc, _, _ = select(tc, op, 0, 0, 0.5, 1)
+    assert sc[0, 2] == -np.inf and np.isfinite(sc[1, 4])
+    sc, _, _ = select(tc, op, 1, 0, 0.5, 1)
+    assert sc[0, 2] == -np.inf and sc[1, 4] == -np.inf
+
+
+SELECTION_CHECKS = [check_select_golden, check_select_nan_reported]
 
 
 # ------------------------------------------------------- verification
@@ -472,6 +526,12 @@ def check_append_hand(append):
         assert np.array_equal(vc2[0, g, 2:5], vs[0, g, [2, 3, 0]])
         assert np.all(kc2[0, g, :2] == -1.0) and np.all(kc2[0, g, 5:] == -1.0)
         assert np.all(vc2[0, g, :2] == -2.0) and np.all(vc2[0, g, 5:] == -2.0)
+    # a slot listed again is committed once: the order [1, 1] appends slot 1's two tokens once
+    kc4, vc4, lens4 = append(kc, vc, [2], ks, vs, acc, np.array([[1, 1]]))
+    assert lens4.tolist() == [4]
+    for g in range(Hkv):
+        assert np.array_equal(kc4[0, g, 2:4], ks[0, g, [2, 3]]) and np.all(kc4[0, g, 4:] == -1.0)
+        assert np.array_equal(vc4[0, g, 2:4], vs[0, g, [2, 3]]) and np.all(vc4[0, g, 4:] == -2.0)
     # the same append into a cache of capacity 4 does not fit: the row is left as it was
     kc3, vc3, lens3 = append(kc[:, :, :4], vc[:, :, :4], [2], ks, vs, acc, np.array([[1, 0]]))
     assert lens3.tolist() == [2] and np.all(kc3 == -1.0) and np.all(vc3 == -2.0)
@@ -588,7 +648,28 @@ def check_sampling_cold_and_prob(sample):
 
 PHILOX_CHECKS = [check_philox_kat]
 UNIFORM_CHECKS = [check_uniform_moments, check_gumbel_moments]
-SAMPLING_CHECKS = [check_sampling_distribution, check_sampling_cold_and_prob]
+def check_sampling_nonfinite_rows(sample):
+    """A row with a NaN or infinite hidden value has no distribution to draw
+    from (scipy's logsumexp of its logits is not finite): sample id -1 and NaN
+    probabilities; the other rows draw what they draw without it."""
+    rng = np.random.default_rng(13)
+    h = rng.standard_normal((5, 16))
+    w = rng.standard_normal((200, 16))
+    clean = sample(h, w, 0.8, seed=3, offset=4)
+    h2 = h.copy()
+    h2[2, 7] = np.nan
+    h2[3, 1] = -np.inf
+    with np.errstate(invalid="ignore", over="ignore"):
+        bad = ~np.isfinite(scipy.special.logsumexp(h2 @ w.T, axis=1))
+    assert bad.tolist() == [False, False, True, True, False]
+    r = sample(h2, w, 0.8, seed=3, offset=4)
+    assert np.all(r["sample_id"][bad] == -1)
+    assert np.all(np.isnan(r["sample_prob"][bad])) and np.all(np.isnan(r["lse"][bad]))
+    assert np.array_equal(r["sample_id"][~bad], clean["sample_id"][~bad])
+    assert np.array_equal(r["sample_prob"][~bad], clean["sample_prob"][~bad])
+
+
+SAMPLING_CHECKS = [check_sampling_distribution, check_sampling_cold_and_prob, check_sampling_nonfinite_rows]
 
 
 # ---------------------------------------------------------------- Mode A (Sec. 5.1)

@@ -140,7 +140,24 @@ def _conf_prob_without_normaliser(h, w, target_ids=None, row_chunk=256):
     return r
 
 
+def _conf_nonfinite_keeps_argmax(h, w, target_ids=None, row_chunk=256):
+    r = oracle.slot_confidence(h, w, target_ids, row_chunk)
+    with np.errstate(invalid="ignore", over="ignore"):
+        logits = np.asarray(h, np.float64) @ np.asarray(w, np.float64).T
+    bad = r["argmax"] < 0
+    r["argmax"][bad] = np.argmax(logits[bad], axis=1)  # numpy's id of the first NaN
+    return r
+
+
+def _conf_nonfinite_rows_dropped_nan(h, w, target_ids=None, row_chunk=256):
+    # NaN hidden values treated as zero
+    return oracle.slot_confidence(np.nan_to_num(np.asarray(h, np.float64), nan=0.0, posinf=0.0), w, target_ids,
+                                  row_chunk)
+
+
 CONFIDENCE_MUTANTS = {
+    "non-finite row keeps numpy's argmax": _conf_nonfinite_keeps_argmax,
+    "non-finite hidden values read as zero": _conf_nonfinite_rows_dropped_nan,
     "argmax takes the highest id on ties": _conf_wrong_tie,
     "lse without the max": _conf_lse_missing_max,
     "vocab rows shifted by one": _conf_shuffled_vocab,
@@ -202,7 +219,26 @@ ATTENTION_MUTANTS["ragged prefix: longest for every row"] = _attn_ragged_uses_ma
 ATTENTION_MUTANTS["ragged prefix: first row's for every row"] = _attn_ragged_first_row
 
 
+def _sel_nan_first(tc, op=None, cr=0, rule=0, threshold=0.9, k=1):
+    tc = np.array(tc, dtype=np.float32)
+    # NaN read as +inf: NaN slots rank first and pass the threshold
+    if cr == oracle.CONF_FIRST_TOKEN:
+        tc[..., 0] = np.where(np.isnan(tc[..., 0]), np.float32(np.inf), tc[..., 0])
+    else:
+        tc = np.where(np.isnan(tc).any(axis=2, keepdims=True), np.float32(np.inf), tc)
+    return oracle.select_slots(tc, op, cr, rule, threshold, k)
+
+
+def _sel_nan_reported(tc, op=None, cr=0, rule=0, threshold=0.9, k=1):
+    c, sel, n = oracle.select_slots(tc, op, cr, rule, threshold, k)
+    conf = oracle.slot_conf(tc, cr)
+    c = np.where(np.isnan(conf) & (c != -1.0), conf, c)  # reports the NaN itself
+    return c, sel, n
+
+
 SELECTION_MUTANTS = {
+    "NaN confidence ranks first": _sel_nan_first,
+    "NaN confidence reported as NaN": _sel_nan_reported,
     "threshold compared with >=": _sel_non_strict,
     "fallback takes the highest index on ties": _sel_fallback_highest_index,
     "output in slot order": _sel_slot_order,
@@ -298,7 +334,33 @@ def _app_keys_for_values(kc, vc, pl, ks, vs, acc, order):
     return oracle.kv_append(kc, vc, pl, ks, ks, acc, order)
 
 
+def _app_repeats_appended(kc, vc, pl, ks, vs, acc, order):
+    # a slot listed twice is appended twice: repeats become distinct copies of the slot
+    order = np.asarray(order)
+    B, S = order.shape
+    L = np.asarray(acc).shape[2]
+    acc2 = np.zeros((B, 2 * S, L), dtype=np.uint8)
+    ks2 = np.concatenate([ks, ks], axis=2)
+    vs2 = np.concatenate([vs, vs], axis=2)
+    order2 = np.full((B, 2 * S), -1, dtype=np.int64)
+    for b in range(B):
+        seen = set()
+        for i, s in enumerate(order[b]):
+            if s < 0:
+                break
+            if s >= S:
+                order2[b, i] = 2 * S
+                continue
+            s2 = int(s) + (S if s in seen else 0)
+            seen.add(int(s))
+            order2[b, i] = s2
+            acc2[b, s2] = np.asarray(acc)[b, s]
+    # slot s2 of the widened layout holds tokens s2*L.., so ks2 must hold slot s at s and s+S
+    return oracle.kv_append(kc, vc, pl, ks2, vs2, acc2, order2)
+
+
 APPEND_MUTANTS = {
+    "a repeated slot appended twice": _app_repeats_appended,
     "slots appended in slot order": _app_slot_order_ignored,
     "appended one position late": _app_off_by_one,
     "partly accepted slots appended whole": _app_whole_slots,
@@ -398,7 +460,20 @@ def _sample_prob_of_argmax(h, w, T, seed, offset, row_chunk=256):
     return r
 
 
+def _sample_nonfinite_drawn(h, w, T, seed, offset, row_chunk=256):
+    # a row without a distribution still reports the id of its best score
+    r = osm.slot_sample(h, w, T, seed, offset, row_chunk)
+    with np.errstate(invalid="ignore", over="ignore"):
+        z = np.asarray(h, np.float64) @ np.asarray(w, np.float64).T
+        u = osm.uniforms(np.arange(z.shape[0]), z.shape[1], seed, offset)
+        score = z / T + osm.gumbel(u)
+    bad = r["sample_id"] < 0
+    r["sample_id"][bad] = np.argmax(score[bad], axis=1)
+    return r
+
+
 SAMPLING_MUTANTS = {
+    "row without a distribution still sampled": _sample_nonfinite_drawn,
     "noise sign flipped": _with_sampling(gum=lambda u: np.log(-np.log(u))),
     "exponential instead of Gumbel noise": _with_sampling(gum=lambda u: -np.log(u)),
     "one word for a whole block": _with_sampling(unif=_unif_block_word0),
