@@ -1,21 +1,28 @@
 #!/usr/bin/env python3
-"""Benchmark one slot-scoring step of Zarya's slotted speculative decoding on one MI355X.
+"""Benchmark the slot-scoring step of Zarya's slotted speculative decoding on one MI355X.
 
 A step (Sec. 5.2 of the paper: draft phase, slot confidence, slot selection)
 is, on one batch of synthetic input already resident in HBM:
 
   1. zarya_slot_attn        DIFFUSION pass (draft) over the prefix cache
   2. zarya_slot_confidence  LM-head confidence of every draft token
-  3. zarya_select_slots     threshold 0.9 on the first-token confidence
+  3. zarya_select_slots     the workload's selection rule (below)
 
-Workload (default): qwen0.6b -- B=16, Hq/Hkv=16/8, D=128, P=2048, S=8, L=8,
-H=1024, V=151936, bf16.  Three copies of the inputs are rotated so that
-neither the KV cache nor the LM head is served from the 256 MB Infinity Cache.
+Headline workload (the JSON line's `value`): qwen4b -- the 4B-scale
+long-context layer, B=8, Hq/Hkv=32/8, D=128, P=16384, S=8, L=16, H=2560,
+V=151936, bf16; selection: threshold 0.9 on the first-token confidence
+(Sec. 5.2, Sec. 6).  The same line carries the qwen0.6b (B=16, 16/8 heads,
+P=2048, S=8, L=8, H=1024; threshold 0.9) and qwen1.7b (B=32, 16/8 heads,
+P=4096, S=16, L=4, H=2048; top-4 slots by mean max-prob) steps under
+`workloads`, each with its own rooflines.  Three copies of every input are
+rotated so that neither the KV cache nor the LM head is served from the
+256 MB Infinity Cache.
 
-Prints one JSON line: steps/s (value), draft tokens/s, per-call times from HIP
-events on the launch stream, the roofline of the dominant kernel
-(slot_confidence against the bf16 MFMA peak) and of slot_attn (against HBM),
-and the float64 CPU oracle timed on the host cores as a reference baseline.
+Times come from HIP events recorded on the stream the library launches on
+(torch's current stream); `roofline` is the dominant kernel's
+(slot_confidence, against the bf16 MFMA peak) and `roofline_slot_attn` the
+attention's, against both the HBM and the MFMA peak.  The float64 CPU oracle
+is timed on the host cores as a reference baseline.
 """
 
 from __future__ import annotations
@@ -36,7 +43,17 @@ if ROOT not in sys.path:
 PEAK_HBM_GBPS = 8000.0
 PEAK_BF16_TFLOPS = 2500.0
 METRIC = "slot-scoring steps/s, draft tokens/s; slot_attn HBM GB/s & conf MFMA % @1 MI355X"
-COUNTERS = os.path.join(ROOT, "profiles", "hbm_traffic_counters.md")
+HEADLINE = "qwen4b"
+SUB_WORKLOADS = ["qwen0.6b", "qwen1.7b"]
+# selection of each workload's step: (slot confidence rule, selection rule, threshold, k)
+SELECTION = {
+    "qwen0.6b": ("first_token", "threshold", 0.9, 1),
+    "qwen1.7b": ("mean", "top_k", 0.9, 4),
+    "qwen4b": ("first_token", "threshold", 0.9, 1),
+}
+# which peak bounds the attention of each workload (algorithmic flops / bytes against the ridge point)
+ATTN_BOUND = {"qwen0.6b": "hbm", "qwen1.7b": "hbm", "qwen4b": "mfma"}
+COUNTERS = os.path.join(ROOT, "profiles", "hbm_traffic_{}.md")
 
 
 def quantile(sorted_vals, q):
@@ -51,31 +68,41 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def conf_source_hash():
-    """sha256 of the sources the confidence kernel is built from (ties the
-    committed counter readings to the kernel version they were taken on)."""
+KERNEL_SOURCES = {
+    "slot_confidence": ("slot_conf.hip", "common.hpp", "kernels.hpp"),
+    "slot_attn": ("slot_attn.hip", "common.hpp", "kernels.hpp"),
+}
+
+
+def source_hash(op):
+    """sha256 of the sources an op's kernels are built from (ties committed
+    counter readings to the kernel version they were taken on)."""
     h = hashlib.sha256()
-    for f in ("slot_conf.hip", "common.hpp", "kernels.hpp"):
+    for f in KERNEL_SOURCES[op]:
         with open(os.path.join(ROOT, "paper_2609_19868_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload):
-    """HBM bytes per slot_confidence launch from the committed rocprofv3
-    counter summary, or None when absent or taken on other kernel sources."""
-    if not os.path.exists(COUNTERS):
+def measured_traffic(workload, op):
+    """HBM bytes per launch of `op` from the committed rocprofv3 counter
+    summary of `workload`, or None when absent or taken on other sources."""
+    path = COUNTERS.format(workload)
+    if not os.path.exists(path):
         return None
-    text = open(COUNTERS).read()
-    m = re.search(r"^source_sha256:\s*(\S+)", text, re.M)
-    t = re.search(rf"^traffic_bytes\[{re.escape(workload)}\]:\s*([0-9.eE+]+)", text, re.M)
-    if not m or not t or m.group(1) != conf_source_hash():
+    text = open(path).read()
+    m = re.search(rf"^source_sha256\[{re.escape(op)}\]:\s*(\S+)", text, re.M)
+    t = re.search(rf"^traffic_bytes\[{re.escape(op)}\]:\s*([0-9.eE+]+)", text, re.M)
+    if not m or not t or m.group(1) != source_hash(op):
         return None
     return float(t.group(1))
 
 
-def cpu_baseline(wl, x, c):
-    """The float64 oracle as it stands, on this host's cores: the whole step."""
+def cpu_baseline(wl, x, c, sel):
+    """The float64 oracle as it stands, on this host's cores: the whole step
+    (attention of every head, confidence of every row over the whole
+    vocabulary, selection).  One run, or the median of three when one run
+    takes under 8 s, so the leg stays within about 10-30 s."""
     import numpy as np
     from threadpoolctl import threadpool_info
 
@@ -85,16 +112,18 @@ def cpu_baseline(wl, x, c):
     xf = {k: W.as_f64(v, wl.dtype) for k, v in x.items()}
     hf = W.as_f64(c["hidden"], wl.dtype)
     wf = W.as_f64(c["w_vocab"], wl.dtype)
+    conf_rule = oracle.CONF_MEAN if sel[0] == "mean" else oracle.CONF_FIRST_TOKEN
+    rule = oracle.SELECT_TOP_K if sel[1] == "top_k" else oracle.SELECT_THRESHOLD
     times = []
-    for rep in range(3):
+    while len(times) < (3 if not times or times[0] < 8.0 else 1):
         t0 = time.perf_counter()
         oracle.slot_attention(xf["q"], xf["k_cache"], xf["v_cache"], xf["k_slot"], xf["v_slot"], wl.prefix_len,
                               wl.n_slots, wl.slot_len, wl.scale, oracle.PASS_DIFFUSION)
         r = oracle.slot_confidence(hf, wf)
         oracle.select_slots(r["max_prob"].reshape(wl.batch, wl.n_slots, wl.slot_len).astype(np.float32), None,
-                            oracle.CONF_FIRST_TOKEN, oracle.SELECT_THRESHOLD, 0.9, 1)
+                            conf_rule, rule, sel[2], sel[3])
         times.append(time.perf_counter() - t0)
-        log(f"cpu oracle step {rep}: {times[-1]:.2f} s")
+        log(f"cpu oracle step {len(times) - 1}: {times[-1]:.2f} s")
     pools = threadpool_info()
     threads = max([d.get("num_threads", 1) for d in pools] + [1])
     blas = ",".join(sorted({d.get("internal_api", "?") for d in pools if d.get("user_api") == "blas"})) or "none"
@@ -104,47 +133,46 @@ def cpu_baseline(wl, x, c):
         "unit": "steps/s",
         "cores": threads,
         "kind": "oracle",
-        "sample": "the whole step (attention of all 16x16 heads x 64 tokens, confidence of all 1024 rows over "
-                  "151936 ids, selection), float64 numpy, median of 3 runs; "
-                  f"host has {len(os.sched_getaffinity(0))} usable cores, BLAS {blas} with {threads} threads",
+        "sample": f"the whole {wl.name} step once per run (attention of all {wl.batch}x{wl.n_q_heads} heads x "
+                  f"{wl.T} tokens over P={wl.prefix_len}, confidence of all {wl.M} rows over {wl.vocab} ids, "
+                  f"selection), float64 numpy, median of {len(times)} run(s); host has "
+                  f"{len(os.sched_getaffinity(0))} usable cores, BLAS {blas} with {threads} threads",
         "seconds_per_step": t,
+        "draft_tokens_per_s": wl.M / t,
     }
 
 
-def main():
-    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="qwen0.6b", choices=["qwen0.6b", "qwen1.7b", "qwen4b"])
-    ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the CPU oracle leg")
-    ap.add_argument("--no-extras", action="store_true", help="skip the AR_INFILL and layout-attention timings")
-    ap.add_argument("--copy-calibration", action="store_true",
-                    help="only run a plain 1 GiB device-to-device copy (scale reference for HBM byte counters)")
-    args = ap.parse_args()
+def attn_work(wl):
+    """Algorithmic bytes and flops of one DIFFUSION-pass slot_attn launch."""
+    B, Hq, Hkv, D, P, T, L = wl.batch, wl.n_q_heads, wl.n_kv_heads, wl.head_dim, wl.prefix_len, wl.T, wl.slot_len
+    nbytes = (2 * B * Hkv * P * D * 2  # prefix K and V, once per GQA group
+              + 2 * B * Hq * T * D * 2  # Q in, O out
+              + 2 * B * Hkv * T * D * 2  # the draft tokens' own K and V
+              + B * Hq * T * 4)  # LSE
+    flops = 4.0 * B * Hq * T * (P + L) * D  # QK^T and PV over the prefix and the row's own slot
+    return nbytes, flops
 
-    world = int(os.environ.get("WORLD_SIZE", "1"))
-    if args.gpus != 1 or world != 1:
-        print("bench.py measures the slot-scoring step on one GPU only; the multi-GPU sharding is designed "
-              "but not built (run with --gpus 1)", file=sys.stderr)
-        sys.exit(2)
 
+def measure_workload(name, steps, warmup, extras, want_cpu):
+    """Time the scoring step of one workload; returns its record (and runs the
+    extras that belong to it)."""
     import numpy as np
     import torch
 
-    import workloads as W
     import paper_2609_19868_amd as Z
+    import workloads as W
+    from paper_2609_19868_amd import _lib
 
     dev = torch.device("cuda:0")
-    if args.copy_calibration:
-        copy_calibration(dev, args.steps)
-        return
-    wl = W.WORKLOADS[args.workload]
+    wl = W.WORKLOADS[name]
     B, Hq, Hkv, D, P, S, L, H, V = (wl.batch, wl.n_q_heads, wl.n_kv_heads, wl.head_dim, wl.prefix_len, wl.n_slots,
                                     wl.slot_len, wl.hidden, wl.vocab)
     T, M = wl.T, wl.M
+    sel = SELECTION[name]
+    conf_rule = Z.SLOT_CONF_MEAN if sel[0] == "mean" else Z.SLOT_CONF_FIRST_TOKEN
+    rule = Z.SELECT_TOP_K if sel[1] == "top_k" else Z.SELECT_THRESHOLD
 
-    log(f"generating {wl.name} inputs")
+    log(f"generating {name} inputs")
     x = W.attention_inputs(wl)
     c = W.confidence_inputs(wl)
 
@@ -160,8 +188,7 @@ def main():
     out = torch.empty((B, Hq, T, D), dtype=torch.bfloat16, device=dev)
     lse = torch.empty((B, Hq, T), dtype=torch.float32, device=dev)
     desc = Z.slot_attn_desc(base["q"], base["k_cache"], base["k_slot"], S, L, Z.PASS_DIFFUSION)
-    from paper_2609_19868_amd import _lib
-
+    plan = _lib.slot_attn_plan(desc)
     attn_ws = torch.empty(max(1, _lib.slot_attn_workspace_size(desc)), dtype=torch.uint8, device=dev)
     conf_out = {
         "max_prob": torch.empty(M, dtype=torch.float32, device=dev),
@@ -183,8 +210,7 @@ def main():
         Z.slot_confidence(s["hidden"], s["w_vocab"], out=conf_out, workspace=conf_ws)
         if evs:
             evs[2].record()
-        Z.select_slots(conf_out["max_prob"].view(B, S, L), None, Z.SLOT_CONF_FIRST_TOKEN, Z.SELECT_THRESHOLD, 0.9, 1,
-                       out=sel_out)
+        Z.select_slots(conf_out["max_prob"].view(B, S, L), None, conf_rule, rule, sel[2], sel[3], out=sel_out)
         if evs:
             evs[3].record()
 
@@ -206,90 +232,153 @@ def main():
             [statistics.median(p[j] for p in per) for j in range(3)], \
             [[quantile(sorted(p[j] for p in per), q) for q in (0.1, 0.9)] for j in range(3)]
 
-    log(f"timing {args.steps} steps after {args.warmup} warm-up steps (DIFFUSION pass)")
-    ms_step, mean_ms, med_ms, pct_ms = timed(Z.PASS_DIFFUSION, args.steps, args.warmup)
+    log(f"{name}: timing {steps} steps after {warmup} warm-up steps (DIFFUSION pass)")
+    ms_step, mean_ms, med_ms, pct_ms = timed(Z.PASS_DIFFUSION, steps, warmup)
     attn_ms, conf_ms, sel_ms = mean_ms
-    log(f"step {ms_step * 1e3:.1f} us: slot_attn {attn_ms * 1e3:.1f} us, slot_confidence {conf_ms * 1e3:.1f} us, "
-        f"select_slots {sel_ms * 1e3:.1f} us")
+    log(f"{name}: step {ms_step * 1e3:.1f} us: slot_attn {attn_ms * 1e3:.1f} us, slot_confidence "
+        f"{conf_ms * 1e3:.1f} us, select_slots {sel_ms * 1e3:.1f} us")
 
-    # algorithmic work (what the method must move / compute once)
-    attn_bytes = (2 * B * Hkv * P * D * 2  # prefix K and V, once per GQA group
-                  + 2 * B * Hq * T * D * 2  # Q in, O out
-                  + 2 * B * Hkv * T * D * 2  # the draft tokens' own K and V
-                  + B * Hq * T * 4)  # LSE
+    attn_bytes, attn_flops = attn_work(wl)
     conf_flops = 2.0 * M * V * H
     conf_tflops = conf_flops / (conf_ms * 1e-3) / 1e12
     attn_gbps = attn_bytes / (attn_ms * 1e-3) / 1e9
-    traffic = measured_traffic(wl.name)
+    attn_tflops = attn_flops / (attn_ms * 1e-3) / 1e12
+    sel_desc = (f"top-{sel[3]} slots by mean max-prob" if sel[1] == "top_k"
+                else f"threshold {sel[2]} on the {sel[0].replace('_', '-')} confidence")
+    rec = {
+        "workload": f"{name}: B={B} Hq/Hkv={Hq}/{Hkv} D={D} P={P} S={S} L={L} H={H} V={V}; step = slot_attn "
+                    f"(DIFFUSION) + slot_confidence + select_slots ({sel_desc})",
+        "steps_per_s": 1e3 / ms_step,
+        "ms_per_step": ms_step,
+        "draft_tokens_per_s": B * S * L * 1e3 / ms_step,
+        "kernel_us": {"slot_attn": attn_ms * 1e3, "slot_confidence": conf_ms * 1e3, "select_slots": sel_ms * 1e3},
+        "kernel_us_median": {"slot_attn": med_ms[0] * 1e3, "slot_confidence": med_ms[1] * 1e3,
+                             "select_slots": med_ms[2] * 1e3},
+        "kernel_us_p10_p90": {k: [pct_ms[j][0] * 1e3, pct_ms[j][1] * 1e3]
+                              for j, k in enumerate(("slot_attn", "slot_confidence", "select_slots"))},
+        "roofline": {
+            "bound": "mfma",
+            "kernel": "slot_confidence (GEMM + fused reduction; launch to launch on its stream)",
+            "achieved": conf_tflops,
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": conf_tflops / PEAK_BF16_TFLOPS,
+            "traffic": measured_traffic(name, "slot_confidence"),
+            "algorithmic_flops_per_launch": conf_flops,
+        },
+        "roofline_slot_attn": {
+            "bound": ATTN_BOUND[name],
+            "hbm": {"achieved": attn_gbps, "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": attn_gbps / PEAK_HBM_GBPS,
+                    "algorithmic_bytes_per_launch": attn_bytes},
+            "mfma": {"achieved": attn_tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": attn_tflops / PEAK_BF16_TFLOPS, "algorithmic_flops_per_launch": attn_flops},
+            "traffic": measured_traffic(name, "slot_attn"),
+            "plan": plan,
+        },
+    }
+    if "graph" in extras:
+        log(f"{name}: timing the same step replayed from HIP graphs")
+        rec["graph_step"] = graph_step(step, sets, steps)
+    if "ar_infill" in extras:
+        log(f"{name}: timing the AR_INFILL (verification) pass")
+        ms_ar, mean_ar, _, _ = timed(Z.PASS_AR_INFILL, max(10, steps // 2), 3)
+        rec["ar_infill_pass"] = {"steps_per_s": 1e3 / ms_ar, "slot_attn_us": mean_ar[0] * 1e3}
+    if "verification" in extras:
+        log(f"{name}: timing the verification step")
+        rec["verification_step"] = verification_step(dev, wl, sets[0], conf_out, sel_out, max(10, steps // 2))
+    if "sampled" in extras:
+        log(f"{name}: timing the sampled LM-head reduction (Gumbel-max, T = 1)")
+        rec["sampled_draft"] = sampled_draft(dev, wl, sets, max(10, steps // 2), conf_ms)
+    if "mode_a" in extras:
+        log("timing a Mode A denoising step")
+        rec["mode_a_step"] = mode_a_step(dev, sets[0]["w_vocab"], max(10, steps // 4))
+    del sets, base
+    torch.cuda.empty_cache()
+    if "single" in extras:
+        log(f"{name}: timing the single-sequence step (batch 1)")
+        rec["single_sequence_step"] = single_sequence_step(dev, wl, max(20, steps // 2))
+    if want_cpu:
+        log(f"{name}: timing the float64 CPU oracle (reference baseline)")
+        rec["cpu_baseline"] = cpu_baseline(wl, x, c, sel)
+    return rec
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default=HEADLINE, choices=["qwen0.6b", "qwen1.7b", "qwen4b"],
+                    help="workload of the headline value")
+    ap.add_argument("--only", action="store_true", help="time the headline workload only (no sub-workloads)")
+    ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the CPU oracle leg")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the graph, AR_INFILL, verification, sampling, Mode A, batch-1 and layout timings")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device-to-device copy (scale reference for HBM byte counters)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures the slot-scoring step on one GPU only; the multi-GPU sharding is designed "
+              "but not built (run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    dev = torch.device("cuda:0")
+    if args.copy_calibration:
+        copy_calibration(dev, args.steps)
+        return
+
+    def extras_of(name):
+        if args.no_extras:
+            return set()
+        if name == args.workload:
+            return {"graph", "ar_infill", "sampled"}
+        if name == "qwen0.6b":
+            return {"verification", "sampled", "mode_a", "single"}
+        return set()
+
+    head = measure_workload(args.workload, args.steps, args.warmup, extras_of(args.workload),
+                            not args.no_cpu_baseline)
+    subs = {}
+    if not args.only:
+        for name in SUB_WORKLOADS + [HEADLINE]:
+            if name != args.workload and name not in subs:
+                subs[name] = measure_workload(name, args.steps, args.warmup, extras_of(name), False)
 
     result = {
         "metric": METRIC,
-        "value": 1e3 / ms_step,
+        "value": head["steps_per_s"],
         "unit": "steps/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms_step,
+        "ms_per_step": head["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded N(0,1) activations and KV cache, N(0,0.02^2) LM head, rounded to bf16)",
         "config": {
-            "workload": f"{wl.name}: B={B} Hq/Hkv={Hq}/{Hkv} D={D} P={P} S={S} L={L} H={H} V={V}; "
-                        "step = slot_attn (DIFFUSION) + slot_confidence + select_slots (threshold 0.9)",
-            "batch": B, "prefix_len": P, "n_slots": S, "slot_len": L, "hidden": H, "vocab": V,
+            "workload": head["workload"],
             "parallelism": "single GPU",
         },
-        "draft_tokens_per_s": B * S * L * 1e3 / ms_step,
-        "kernel_us": {"slot_attn": attn_ms * 1e3, "slot_confidence": conf_ms * 1e3, "select_slots": sel_ms * 1e3},
-        "kernel_us_median": {"slot_attn": med_ms[0] * 1e3, "slot_confidence": med_ms[1] * 1e3,
-                             "select_slots": med_ms[2] * 1e3},
-        "kernel_us_p10_p90": {name: [pct_ms[j][0] * 1e3, pct_ms[j][1] * 1e3]
-                              for j, name in enumerate(("slot_attn", "slot_confidence", "select_slots"))},
-        "roofline": {
-            "bound": "mfma",
-            "kernel": "slot_confidence (GEMM + fused reduction, plus its partial-merge kernel)",
-            "achieved": conf_tflops,
-            "peak": PEAK_BF16_TFLOPS,
-            "unit": "TFLOP/s",
-            "frac": conf_tflops / PEAK_BF16_TFLOPS,
-            "traffic": traffic,
-            "algorithmic_flops_per_launch": conf_flops,
-        },
-        "roofline_slot_attn": {
-            "bound": "hbm",
-            "achieved": attn_gbps,
-            "peak": PEAK_HBM_GBPS,
-            "unit": "GB/s",
-            "frac": attn_gbps / PEAK_HBM_GBPS,
-            "algorithmic_bytes_per_launch": attn_bytes,
-            "prefix_splits": max(1, round(_lib.slot_attn_workspace_size(desc) / (B * Hq * T * (D + 1) * 4))),
-        },
+        "draft_tokens_per_s": head["draft_tokens_per_s"],
+        "roofline": head["roofline"],
+        "roofline_slot_attn": head["roofline_slot_attn"],
     }
-
+    if "cpu_baseline" in head:
+        result["cpu_baseline"] = head.pop("cpu_baseline")
+    for k in ("kernel_us", "kernel_us_median", "kernel_us_p10_p90", "graph_step", "ar_infill_pass",
+              "sampled_draft"):
+        if k in head:
+            result[k] = head[k]
+    if subs:
+        result["workloads"] = subs
     if not args.no_extras:
-        log("timing the same step replayed from HIP graphs")
-        result["graph_step"] = graph_step(step, sets, args.steps)
-        log("timing the AR_INFILL (verification) pass")
-        ms_ar, mean_ar, _, _ = timed(Z.PASS_AR_INFILL, max(10, args.steps // 2), 3)
-        result["ar_infill_pass"] = {"steps_per_s": 1e3 / ms_ar, "slot_attn_us": mean_ar[0] * 1e3}
-        log("timing the verification step")
-        result["verification_step"] = verification_step(dev, wl, sets[0], conf_out, sel_out, max(10, args.steps // 2))
-        log("timing the sampled LM-head reduction (Gumbel-max, T = 1)")
-        result["sampled_draft"] = sampled_draft(dev, wl, sets, max(10, args.steps // 2), conf_ms)
-        if wl.hidden == W.WORKLOADS["modeA"].hidden:
-            log("timing a Mode A denoising step")
-            result["mode_a_step"] = mode_a_step(dev, sets[0]["w_vocab"], max(10, args.steps // 4))
-        del sets
-        torch.cuda.empty_cache()
-        log("timing the single-sequence step (batch 1)")
-        result["single_sequence_step"] = single_sequence_step(dev, wl, max(20, args.steps // 2))
         result["layout_attention"] = layout_attention(dev, max(5, args.steps // 10))
-
-    if not args.no_cpu_baseline:
-        log("timing the float64 CPU oracle (reference baseline)")
-        result["cpu_baseline"] = cpu_baseline(wl, x, c)
     print(json.dumps(result), flush=True)
 
 

@@ -136,6 +136,17 @@ typedef struct zarya_slot_attn_desc {
 /* Bytes of device workspace zarya_slot_attn needs for `desc` (may be 0). */
 zarya_status zarya_slot_attn_workspace_size(const zarya_slot_attn_desc* desc, size_t* bytes);
 
+/* Work decomposition zarya_slot_attn chooses for `desc` (diagnostics only;
+ * nothing is launched).  Host memory `info` is filled on ZARYA_OK. */
+typedef struct zarya_slot_attn_plan_info {
+  int32_t prefix_splits;      /* ranges of prefix keys given to separate workgroups (1 = none) */
+  int32_t rows_per_workgroup; /* query rows (of one GQA group) per workgroup                 */
+  int32_t workgroups;         /* workgroups of the attention kernel                          */
+  int32_t kernels;            /* kernels one call enqueues                                   */
+} zarya_slot_attn_plan_info;
+
+zarya_status zarya_slot_attn_plan(const zarya_slot_attn_desc* desc, zarya_slot_attn_plan_info* info);
+
 /*
  * q         [B, Hq, T, D]  dtype   draft-token queries, T = S*L, row t = s*L + r
  * k_cache   [B, Hkv, C, D] dtype   prefix keys; rows >= P are never read;
@@ -170,7 +181,10 @@ zarya_status zarya_slot_attn(const zarya_slot_attn_desc* desc, const void* q, co
  *   lse[i]         = ln sum_v exp(z_v)
  *   max_prob[i]    = exp(max_v z_v - lse[i])   (largest softmax probability)
  *   target_prob[i] = exp(z_{target_ids[i]} - lse[i])
- * Logits are computed in float32 and never written to memory.
+ * Logits are computed in float32 and never written to memory.  A row whose
+ * logits include a NaN or an infinity (a NaN or infinite value in its hidden
+ * state, say) has no softmax -- its log-sum-exp is not finite -- and reports
+ * argmax_id -1 and NaN for max_prob, lse and target_prob.
  */
 typedef struct zarya_conf_desc {
   int32_t n_rows; /* M >= 1                                              */
@@ -220,6 +234,9 @@ typedef enum zarya_select_rule {
  *                                 confidence, ties to the lower slot index), then -1
  * n_selected  [B] int32 out       number of chosen slots
  * Comparisons are made between float32 values; `threshold` is used as given.
+ * A NaN slot confidence counts as -inf: it ranks after every other open slot
+ * (ties among such slots go to the lower index), never exceeds the threshold,
+ * and is reported as -inf in slot_conf.
  * Requires 1 <= S <= 1024 and k >= 0 for TOP_K.
  */
 zarya_status zarya_select_slots(int32_t batch, int32_t n_slots, int32_t slot_len, const float* token_conf,
@@ -283,7 +300,9 @@ typedef struct zarya_kv_append_desc {
  * k_slot, v_slot   [B, Hkv, S*L, D] dtype  the draft tokens' own K/V
  * accepted         [B, S, L] uint8         nonzero = append
  * order            [B, S] int32            slots in append order (e.g. `selected`);
- *                                          ids outside [0, S) are skipped
+ *                                          ids outside [0, S) are skipped, and
+ *                                          so is a slot listed a second time
+ *                                          (its tokens are appended once)
  * prefix_lens      [B] int32 in/out
  * k_cache, v_cache [B, Hkv, C, D] dtype in/out
  * A row whose prefix_lens[b] is negative or whose append would pass C is left
@@ -312,7 +331,8 @@ zarya_status zarya_kv_append(const zarya_kv_append_desc* desc, const void* k_slo
  * offset, i, v): advance `offset` between draft steps for fresh noise.  The
  * perturbed scores are compared in float32 (in base 2:
  * z log2(e) / T - log2(-log2 u), the same order).  Logits are never written to
- * memory.
+ * memory.  A row whose logits include a NaN or an infinity has no
+ * distribution to draw from: sample_id -1, NaN sample_prob, max_prob and lse.
  */
 typedef struct zarya_sample_params {
   float temperature; /* T: finite, > 0                                      */

@@ -85,11 +85,31 @@ def _stream(dev):
 
 
 def _need(t, name, shape, dtype, device):
+    if t.device.type != "cuda":
+        raise ValueError(f"{name}: expected a cuda (HIP) device tensor, got one on {t.device}")
     if t.device != device or t.dtype != dtype or tuple(t.shape) != tuple(shape) or not t.is_contiguous():
         raise ValueError(
             f"{name}: expected contiguous {dtype} {tuple(shape)} on {device}, "
             f"got {t.dtype} {tuple(t.shape)} on {t.device} (contiguous={t.is_contiguous()})"
         )
+
+
+def _need_opt(t, name, shape, dtype, device):
+    if t is not None:
+        _need(t, name, shape, dtype, device)
+
+
+def _need_workspace(ws, n_bytes, device):
+    """A caller's workspace: a contiguous 1-D uint8 device tensor of at least n_bytes."""
+    if ws is None:
+        return
+    if ws.device.type != "cuda":
+        raise ValueError(f"workspace: expected a cuda (HIP) device tensor, got one on {ws.device}")
+    if ws.device != device or ws.dtype != torch.uint8 or ws.dim() != 1 or not ws.is_contiguous():
+        raise ValueError(f"workspace: expected a contiguous 1-D torch.uint8 tensor on {device}, "
+                         f"got {ws.dtype} {tuple(ws.shape)} on {ws.device} (contiguous={ws.is_contiguous()})")
+    if ws.numel() < n_bytes:
+        raise ValueError(f"workspace: {ws.numel()} bytes, {n_bytes} required")
 
 
 def slot_attn_desc(q, k_cache, k_slot, n_slots, slot_len, pass_=PASS_DIFFUSION, cross_slot=CROSS_SLOT_NONE,
@@ -142,6 +162,7 @@ def slot_attn(q, k_cache, v_cache, k_slot, v_slot, n_slots, slot_len, pass_=PASS
     if lse is not None:
         _need(lse, "lse", (B, Hq, T), torch.float32, dev)
     ws_bytes = _lib.slot_attn_workspace_size(desc)
+    _need_workspace(workspace, ws_bytes, dev)
     if workspace is None and ws_bytes > 0:
         workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     with torch.cuda.device(dev):  # the library launches on the current device
@@ -175,7 +196,12 @@ def slot_confidence(hidden, w_vocab, target_ids=None, out=None, workspace=None):
         }
         if target_ids is not None:
             out["target_prob"] = torch.empty(M, dtype=torch.float32, device=dev)
+    _need(out["max_prob"], "out['max_prob']", (M,), torch.float32, dev)
+    _need(out["argmax"], "out['argmax']", (M,), torch.int32, dev)
+    _need_opt(out.get("lse"), "out['lse']", (M,), torch.float32, dev)
+    _need_opt(out.get("target_prob"), "out['target_prob']", (M,), torch.float32, dev)
     ws_bytes = _lib.slot_confidence_workspace_size(desc)
+    _need_workspace(workspace, ws_bytes, dev)
     if workspace is None:
         workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     with torch.cuda.device(dev):  # the library launches on the current device
@@ -211,7 +237,12 @@ def slot_sample(hidden, w_vocab, temperature, seed, offset=0, rows=None, out=Non
     if out is None:
         out = {k: torch.empty(M, dtype=torch.float32, device=dev) for k in ("sample_prob", "max_prob", "lse")}
         out["sample_id"] = torch.empty(M, dtype=torch.int32, device=dev)
+    _need(out["sample_id"], "out['sample_id']", (M,), torch.int32, dev)
+    _need(out["sample_prob"], "out['sample_prob']", (M,), torch.float32, dev)
+    _need_opt(out.get("max_prob"), "out['max_prob']", (M,), torch.float32, dev)
+    _need_opt(out.get("lse"), "out['lse']", (M,), torch.float32, dev)
     ws_bytes = _lib.slot_sample_workspace_size(desc)
+    _need_workspace(workspace, ws_bytes, dev)
     if workspace is None:
         workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     with torch.cuda.device(dev):  # the library launches on the current device
@@ -255,6 +286,8 @@ def mdm_reveal(mask, k, rule=REVEAL_CONFIDENCE, conf=None, seed=0, offset=0, sam
     if out is None:
         out = (torch.empty((B, N), dtype=torch.int32, device=dev), torch.empty((B,), dtype=torch.int32, device=dev))
     order, n = out
+    _need(order, "out[0] (order)", (B, N), torch.int32, dev)
+    _need_opt(n, "out[1] (n_revealed)", (B,), torch.int32, dev)
     with torch.cuda.device(dev):  # the library launches on the current device
         _lib.check(_lib.lib().zarya_mdm_reveal(
             B, N, _ptr(conf), _ptr(mask), _ptr(k), int(rule), int(seed) & (2**64 - 1), int(offset) & (2**64 - 1),
@@ -280,6 +313,9 @@ def select_slots(token_conf, slot_open=None, conf_rule=SLOT_CONF_FIRST_TOKEN, ru
             torch.empty((B,), dtype=torch.int32, device=dev),
         )
     slot_conf, selected, n_selected = out
+    _need(slot_conf, "out[0] (slot_conf)", (B, S), torch.float32, dev)
+    _need(selected, "out[1] (selected)", (B, S), torch.int32, dev)
+    _need(n_selected, "out[2] (n_selected)", (B,), torch.int32, dev)
     with torch.cuda.device(dev):  # the library launches on the current device
         _lib.check(_lib.lib().zarya_select_slots(
             B, S, L, _ptr(token_conf), _ptr(slot_open), int(conf_rule), int(rule), float(threshold), int(k),
@@ -306,6 +342,9 @@ def verify_accept(token_prob, selected, token_threshold=0.4, rule=ACCEPT_PREFIX,
             torch.empty((B,), dtype=torch.int32, device=dev),
         )
     accepted, n_accepted, n_total = out
+    _need(accepted, "out[0] (accepted)", (B, S, L), torch.uint8, dev)
+    _need(n_accepted, "out[1] (n_accepted)", (B, S), torch.int32, dev)
+    _need_opt(n_total, "out[2] (n_total)", (B,), torch.int32, dev)
     with torch.cuda.device(dev):  # the library launches on the current device
         _lib.check(_lib.lib().zarya_verify_accept(
             B, S, L, _ptr(token_prob), _ptr(selected), float(token_threshold), int(rule), _ptr(accepted),

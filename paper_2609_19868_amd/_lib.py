@@ -39,6 +39,7 @@ REVEAL_RANDOM = 2
 # every symbol include/zarya.h declares
 EXPORTS = (
     "zarya_slot_attn_workspace_size",
+    "zarya_slot_attn_plan",
     "zarya_slot_attn",
     "zarya_slot_confidence_workspace_size",
     "zarya_slot_confidence",
@@ -70,6 +71,15 @@ class SlotAttnDesc(ctypes.Structure):
         ("cross_slot", ctypes.c_int32),
         ("dtype", ctypes.c_int32),
         ("prefix_splits", ctypes.c_int32),
+    ]
+
+
+class SlotAttnPlanInfo(ctypes.Structure):
+    _fields_ = [
+        ("prefix_splits", ctypes.c_int32),
+        ("rows_per_workgroup", ctypes.c_int32),
+        ("workgroups", ctypes.c_int32),
+        ("kernels", ctypes.c_int32),
     ]
 
 
@@ -124,6 +134,8 @@ def lib():
         vp, sz, i32, f32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32, ctypes.c_float
         L.zarya_slot_attn_workspace_size.argtypes = [ctypes.POINTER(SlotAttnDesc), ctypes.POINTER(sz)]
         L.zarya_slot_attn_workspace_size.restype = ctypes.c_int
+        L.zarya_slot_attn_plan.argtypes = [ctypes.POINTER(SlotAttnDesc), ctypes.POINTER(SlotAttnPlanInfo)]
+        L.zarya_slot_attn_plan.restype = ctypes.c_int
         L.zarya_slot_attn.argtypes = [ctypes.POINTER(SlotAttnDesc), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         L.zarya_slot_attn.restype = ctypes.c_int
         L.zarya_slot_confidence_workspace_size.argtypes = [ctypes.POINTER(ConfDesc), ctypes.POINTER(sz)]
@@ -169,6 +181,13 @@ def slot_attn_workspace_size(desc: SlotAttnDesc) -> int:
     n = ctypes.c_size_t(0)
     check(lib().zarya_slot_attn_workspace_size(ctypes.byref(desc), ctypes.byref(n)))
     return n.value
+
+
+def slot_attn_plan(desc: SlotAttnDesc) -> dict:
+    """The work decomposition zarya_slot_attn chooses for desc."""
+    info = SlotAttnPlanInfo()
+    check(lib().zarya_slot_attn_plan(ctypes.byref(desc), ctypes.byref(info)))
+    return {name: int(getattr(info, name)) for name, _ in SlotAttnPlanInfo._fields_}
 
 
 def slot_confidence_workspace_size(desc: ConfDesc) -> int:

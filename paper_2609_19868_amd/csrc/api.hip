@@ -272,6 +272,25 @@ zarya_status zarya_slot_attn_workspace_size(const zarya_slot_attn_desc* desc, si
   return ZARYA_OK;
 }
 
+zarya_status zarya_slot_attn_plan(const zarya_slot_attn_desc* desc, zarya_slot_attn_plan_info* info) {
+  if (!info) return fail(ZARYA_ERR_INVALID_ARGUMENT, "info is NULL");
+  zarya_status st = check_attn_desc(desc);
+  if (st != ZARYA_OK) return st;
+  const AttnPlan pl = plan_attn(desc);
+  if (desc->dtype == ZARYA_DTYPE_F32) {
+    info->prefix_splits = 1;
+    info->rows_per_workgroup = kAttnF32RowsPerBlock;
+    info->workgroups = (int32_t)((pl.rows_total + kAttnF32RowsPerBlock - 1) / kAttnF32RowsPerBlock);
+    info->kernels = 1;
+    return ZARYA_OK;
+  }
+  info->prefix_splits = pl.n_split;
+  info->rows_per_workgroup = pl.rows_per_block;
+  info->workgroups = (int32_t)((int64_t)desc->batch * desc->n_kv_heads * pl.n_split * pl.n_rb);
+  info->kernels = pl.n_split > 1 ? 2 : 1;
+  return ZARYA_OK;
+}
+
 zarya_status zarya_slot_attn(const zarya_slot_attn_desc* d, const void* q, const void* k_cache, const void* v_cache,
                              const void* k_slot, const void* v_slot, const uint8_t* slot_pass,
                              const int32_t* prefix_lens, void* out, float* lse, void* workspace,

@@ -449,8 +449,8 @@ __global__ __launch_bounds__(256) void slot_attn_merge_kernel(const float* __res
 // float32 path: one thread per query row, plain FMA arithmetic, online softmax
 // with expf.  Serves small float32 problems and every mask variant.
 template <int D>
-__global__ __launch_bounds__(64) void slot_attn_f32_kernel(AttnParams32 p) {
-  const int gid = blockIdx.x * 64 + threadIdx.x;
+__global__ __launch_bounds__(kAttnF32RowsPerBlock) void slot_attn_f32_kernel(AttnParams32 p) {
+  const int gid = blockIdx.x * kAttnF32RowsPerBlock + threadIdx.x;
   if (gid >= p.rows_total) return;
   const int t = gid % p.T;
   const int h = (gid / p.T) % p.Hq;
@@ -526,11 +526,11 @@ hipError_t launch_slot_attn_bf16(const AttnParams& p, int head_dim, hipStream_t 
 }
 
 hipError_t launch_slot_attn_f32(const AttnParams32& p, int head_dim, hipStream_t stream) {
-  const int grid = (p.rows_total + 63) / 64;
+  const int grid = (p.rows_total + kAttnF32RowsPerBlock - 1) / kAttnF32RowsPerBlock;
   if (head_dim == 128) {
-    hipLaunchKernelGGL(slot_attn_f32_kernel<128>, dim3(grid), dim3(64), 0, stream, p);
+    hipLaunchKernelGGL(slot_attn_f32_kernel<128>, dim3(grid), dim3(kAttnF32RowsPerBlock), 0, stream, p);
   } else {
-    hipLaunchKernelGGL(slot_attn_f32_kernel<64>, dim3(grid), dim3(64), 0, stream, p);
+    hipLaunchKernelGGL(slot_attn_f32_kernel<64>, dim3(grid), dim3(kAttnF32RowsPerBlock), 0, stream, p);
   }
   return hipGetLastError();
 }

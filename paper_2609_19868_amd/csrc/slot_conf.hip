@@ -643,20 +643,28 @@ __global__ __launch_bounds__(256) void slot_conf_merge_kernel(ConfMergeParams p)
     }
   }
   const float lse2 = m * kLog2e + __log2f(s);
-  const bool tgt_ok = tgt >= 0 && tgt < p.V;
+  // A row whose logits include a NaN or an infinity has no softmax: its sum
+  // is NaN (or 0 when every logit is -inf), so its log-sum-exp is not finite.
+  // Such a row reports id -1 and NaN probabilities, and no logit is recomputed
+  // for it (its ids are not meaningful).  Every lane holds the same merged
+  // statistics, so these conditions are uniform over the wave, as the dot
+  // products' shuffles need.
+  const bool no_softmax = !(fabsf(lse2) < INFINITY);
+  const bool tgt_ok = tgt >= 0 && tgt < p.V && !no_softmax;
+  const bool idx_ok = idx >= 0 && idx < p.V && !no_softmax;
+  const bool sgi_ok = sgi >= 0 && sgi < p.V && !no_softmax;
   const float zt = tgt_ok ? row_logit(p, hrow, tgt, lane) : 0.f;
-  // every row has a finite perturbed score, so sgi is a valid id
-  const float zs = p.part_g ? row_logit(p, hrow, sgi, lane) : 0.f;
+  const float zs = p.part_g && sgi_ok ? row_logit(p, hrow, sgi, lane) : 0.f;
   if (lane != 0) return;
   // a row index outside the hidden rows was clamped for the loads: mark its results
-  const bool bad = p.row_index && (p.row_index[row] < 0 || p.row_index[row] >= p.hidden_rows);
+  const bool bad = no_softmax || (p.row_index && (p.row_index[row] < 0 || p.row_index[row] >= p.hidden_rows));
   const float nan = __builtin_nanf("");
   if (p.max_prob) p.max_prob[row] = bad ? nan : 1.f / s;
-  if (p.argmax_id) p.argmax_id[row] = bad ? -1 : idx;
+  if (p.argmax_id) p.argmax_id[row] = bad || !idx_ok ? -1 : idx;
   if (p.lse) p.lse[row] = bad ? nan : lse2 * kLn2;
   if (p.part_g) {
-    p.sample_id[row] = bad ? -1 : sgi;
-    p.sample_prob[row] = bad ? nan : fast_exp2(zs * kLog2e - lse2);
+    p.sample_id[row] = bad || !sgi_ok ? -1 : sgi;
+    p.sample_prob[row] = bad || !sgi_ok ? nan : fast_exp2(zs * kLog2e - lse2);
   }
   if (p.target_ids && p.target_prob) p.target_prob[row] = tgt_ok && !bad ? fast_exp2(zt * kLog2e - lse2) : nan;
 }

@@ -67,26 +67,35 @@ __global__ __launch_bounds__(kThreads) void verify_accept_kernel(AcceptParams p)
 }
 
 // One workgroup per batch row: list the accepted tokens in append order in
-// LDS, check that they fit, then copy their K and V rows of every KV head in
-// 16-byte pieces and move the row's prefix length.
+// LDS (a slot listed twice counts at its first position only), check that
+// they fit, then copy their K and V rows of every KV head in 16-byte pieces
+// and move the row's prefix length.
 __global__ __launch_bounds__(kThreads) void kv_append_kernel(AppendParams p) {
   __shared__ int slot_of[1024];   // order position -> slot id (or -1)
   __shared__ int count_of[1024];  // order position -> accepted tokens of that slot
   __shared__ int start_of[1024];  // order position -> first index in `tokens`
+  __shared__ int first_pos[1024];  // slot id -> first order position listing it
   __shared__ int tokens[kAppendMaxTokens];
   __shared__ int n_tok, p0, ok;
   const int b = blockIdx.x;
   const int tid = threadIdx.x;
   const int32_t* ord = p.order + (size_t)b * p.S;
   if (tid == 0) n_tok = p.S;
+  for (int s = tid; s < p.S; s += kThreads) first_pos[s] = p.S;
   __syncthreads();
   for (int i = tid; i < p.S; i += kThreads)
     if (ord[i] < 0) atomicMin(&n_tok, i);  // end of the order list
   __syncthreads();
   const int n_pos = n_tok;
+  for (int i = tid; i < n_pos; i += kThreads) {
+    const int s = ord[i];
+    if (s < p.S) atomicMin(&first_pos[s], i);  // LDS integer minimum: order-free
+  }
+  __syncthreads();
   for (int i = tid; i < p.S; i += kThreads) {
     const int s = i < n_pos ? ord[i] : -1;
-    const bool valid = s >= 0 && s < p.S;
+    // a slot listed again is skipped: its tokens are committed once
+    const bool valid = s >= 0 && s < p.S && first_pos[s] == i;
     int c = 0;
     if (valid) {
       const uint8_t* a = p.accepted + ((size_t)b * p.S + s) * p.L;

@@ -10,6 +10,80 @@ import torch
 import workloads as W
 
 
+def run_parallel(fn, items, workers=8):
+    """fn over items on a thread pool, results in order.  The oracle's numpy
+    work (BLAS products, ufuncs over large arrays) releases the GIL, so
+    independent batch rows or row blocks run side by side; BLAS is held to
+    two threads per worker meanwhile."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    from threadpoolctl import threadpool_limits
+
+    with threadpool_limits(limits=2):
+        with ThreadPoolExecutor(max_workers=workers) as ex:
+            return list(ex.map(fn, items))
+
+
+def oracle_attention_by_row(xf, prefix_len, n_slots, slot_len, scale, pass_, cross=0, slot_pass=None):
+    """oracle.slot_attention over every batch row, one row per task (the
+    oracle treats batch rows independently)."""
+    import oracle
+
+    B = xf["q"].shape[0]
+    plens = np.broadcast_to(np.asarray(prefix_len), (B,))
+
+    def one(b):
+        return oracle.slot_attention(xf["q"][b:b + 1], xf["k_cache"][b:b + 1], xf["v_cache"][b:b + 1],
+                                     xf["k_slot"][b:b + 1], xf["v_slot"][b:b + 1], [int(plens[b])], n_slots,
+                                     slot_len, scale, pass_, cross_slot=cross,
+                                     slot_pass=None if slot_pass is None else slot_pass[b:b + 1])
+
+    res = run_parallel(one, range(B))
+    return np.concatenate([r[0] for r in res]), np.concatenate([r[1] for r in res])
+
+
+def _by_blocks(fn, M, block=128):
+    blocks = [(r0, min(M, r0 + block)) for r0 in range(0, M, block)]
+    parts = run_parallel(fn, blocks)
+    return {k: np.concatenate([p[k] for p in parts]) for k in parts[0]}
+
+
+def oracle_confidence_by_block(hf, wf, target_ids=None):
+    """oracle.slot_confidence over every row, blocks of rows side by side (the
+    oracle treats rows independently)."""
+    import oracle
+
+    return _by_blocks(lambda r: oracle.slot_confidence(
+        hf[r[0]:r[1]], wf, target_ids=None if target_ids is None else target_ids[r[0]:r[1]]), hf.shape[0])
+
+
+def oracle_sample_by_block(hf, wf, T, seed, offset, row_ids=None):
+    """oracle.slot_sample over every row, blocks of rows side by side; each
+    row keeps its own index in the random stream."""
+    import oracle
+
+    ids = np.arange(hf.shape[0]) if row_ids is None else np.asarray(row_ids)
+    return _by_blocks(lambda r: oracle.slot_sample(hf[r[0]:r[1]], wf, T, seed, offset, row_ids=ids[r[0]:r[1]]),
+                      hf.shape[0])
+
+
+_FULL_CACHE = {}
+
+
+def full_attention_inputs(wl, dev):
+    """(storage arrays, device tensors, float64 arrays) of a workload's
+    attention inputs; the last workload drawn is kept, so the tests of its two
+    passes draw it once."""
+    key = (wl, str(dev))
+    if key not in _FULL_CACHE:
+        _FULL_CACHE.clear()
+        x = W.attention_inputs(wl)
+        xd = {k: to_dev(v, wl.dtype, dev) for k, v in x.items()}
+        xf = {k: W.as_f64(v, wl.dtype) for k, v in x.items()}
+        _FULL_CACHE[key] = (x, xd, xf)
+    return _FULL_CACHE[key]
+
+
 def require_gpu():
     if not torch.cuda.is_available():
         raise RuntimeError("this test needs an MI355X (HIP device); run the CPU suite with -m 'not gpu'")

@@ -8,6 +8,8 @@ import subprocess
 
 import pytest
 
+import workloads as W
+
 from paper_2609_19868_amd import _lib
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -89,6 +91,27 @@ def test_slot_attn_rejects_null_pointers_and_small_workspace():
     p = ctypes.c_void_p(1)
     assert _lib.lib().zarya_slot_attn(ctypes.byref(d), p, None, None, p, p, None, None, p, None, p, 1 << 40,
                                       None) == _lib.ERR_INVALID_ARGUMENT
+
+
+def test_slot_attn_plan_reports_the_decomposition():
+    """The planner's choice, as zarya_slot_attn_plan reports it, is consistent
+    with the workspace it asks for and covers every GQA group."""
+    for name in ("qwen0.6b", "qwen1.7b", "qwen4b"):
+        wl = W.WORKLOADS[name]
+        d = _lib.SlotAttnDesc(batch=wl.batch, n_q_heads=wl.n_q_heads, n_kv_heads=wl.n_kv_heads, head_dim=128,
+                              prefix_len=wl.prefix_len, kv_capacity=wl.prefix_len, n_slots=wl.n_slots,
+                              slot_len=wl.slot_len, softmax_scale=0.088, pass_=0, cross_slot=0, dtype=1)
+        plan = _lib.slot_attn_plan(d)
+        groups = wl.batch * wl.n_kv_heads
+        rows = wl.n_q_heads // wl.n_kv_heads * wl.T
+        rb = -(-rows // plan["rows_per_workgroup"])
+        assert plan["workgroups"] == groups * rb * plan["prefix_splits"], (name, plan)
+        assert 1 <= plan["prefix_splits"] <= 64 and plan["kernels"] in (1, 2)
+        assert (_lib.slot_attn_workspace_size(d) > 0) == (plan["prefix_splits"] > 1)
+    d = _lib.SlotAttnDesc(batch=1, n_q_heads=2, n_kv_heads=1, head_dim=64, prefix_len=64, kv_capacity=64,
+                          n_slots=4, slot_len=4, softmax_scale=0.125, pass_=0, cross_slot=0, dtype=0)
+    assert _lib.slot_attn_plan(d) == {"prefix_splits": 1, "rows_per_workgroup": 64, "workgroups": 1, "kernels": 1}
+    assert _lib.lib().zarya_slot_attn_plan(ctypes.byref(d), None) == _lib.ERR_INVALID_ARGUMENT
 
 
 def test_slot_attn_workspace_sizes():
@@ -262,3 +285,50 @@ def test_binding_refuses_host_tensors():
         Z.slot_confidence(h, w)
     with pytest.raises(ValueError, match="cuda"):
         Z.select_slots(torch.zeros(2, 3, 4))
+    # caller-supplied outputs and workspaces are checked like the inputs
+    with pytest.raises(ValueError, match="cuda"):
+        Z._need(torch.zeros(4), "out['max_prob']", (4,), torch.float32, torch.device("cpu"))
+    with pytest.raises(ValueError, match="cuda"):
+        Z._need_workspace(torch.zeros(64, dtype=torch.uint8), 16, torch.device("cpu"))
+
+
+def test_binding_checks_workspace_shape_and_size():
+    """A workspace must be a contiguous 1-D uint8 tensor of at least the
+    reported size (its element count is passed as the byte count).  The
+    checks are exercised on a stand-in device object, since this host has no
+    HIP device: only their logic is under test."""
+    import torch
+    import paper_2609_19868_amd as Z
+
+    class FakeCuda:
+        """Tensor stand-in whose device reads as cuda:0."""
+
+        def __init__(self, t):
+            self.t = t
+            self.device = torch.device("cuda:0")
+            self.dtype = t.dtype
+            self.shape = t.shape
+
+        def dim(self):
+            return self.t.dim()
+
+        def is_contiguous(self):
+            return self.t.is_contiguous()
+
+        def numel(self):
+            return self.t.numel()
+
+    dev = torch.device("cuda:0")
+    Z._need_workspace(FakeCuda(torch.zeros(64, dtype=torch.uint8)), 64, dev)  # accepted
+    with pytest.raises(ValueError, match="uint8"):
+        Z._need_workspace(FakeCuda(torch.zeros(64, dtype=torch.float32)), 16, dev)
+    with pytest.raises(ValueError, match="required"):
+        Z._need_workspace(FakeCuda(torch.zeros(15, dtype=torch.uint8)), 16, dev)
+    with pytest.raises(ValueError, match="uint8"):
+        Z._need_workspace(FakeCuda(torch.zeros(4, 16, dtype=torch.uint8)), 16, dev)
+    with pytest.raises(ValueError, match="uint8"):
+        Z._need_workspace(FakeCuda(torch.zeros(64, dtype=torch.uint8)[::2]), 16, dev)
+    with pytest.raises(ValueError, match="expected contiguous"):
+        Z._need(FakeCuda(torch.zeros(5, dtype=torch.float32)), "out['lse']", (4,), torch.float32, dev)
+    with pytest.raises(ValueError, match="expected contiguous"):
+        Z._need(FakeCuda(torch.zeros(4, dtype=torch.int64)), "out['argmax']", (4,), torch.int32, dev)

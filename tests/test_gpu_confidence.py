@@ -13,7 +13,7 @@ import torch
 
 import oracle
 import workloads as W
-from gpu_helpers import check_conf, require_gpu, say, to_dev
+from gpu_helpers import check_conf, oracle_confidence_by_block, require_gpu, say, to_dev
 
 import paper_2609_19868_amd as Z
 
@@ -87,6 +87,52 @@ def test_bf16_zero_hidden_rows():
     np.testing.assert_allclose(res["max_prob"].cpu().numpy(), 1.0 / V, rtol=1e-5)
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_nonfinite_rows_report_minus_one_and_nan(dtype):
+    """Rows with a NaN or infinite hidden value have no softmax: argmax -1 and
+    NaN max_prob / lse / target_prob (greedy), sample id -1 and NaN
+    probabilities (sampled); every other row matches the oracle.  (Before the
+    rule, such a row's sampled id stayed unset and its logit was recomputed
+    from outside the LM head.)"""
+    dev = require_gpu()
+    over = dict(batch=1, n_slots=70, slot_len=4, hidden=256, vocab=5003) if dtype == "bf16" else \
+        dict(batch=1, n_slots=6, slot_len=4, hidden=64, vocab=700)
+    wl = W.WORKLOADS["qwen0.6b" if dtype == "bf16" else "tiny"].replace(**over, seed=95)
+    c = W.confidence_inputs(wl)
+    hidden = c["hidden"].copy()
+    nan_bits = np.uint16(0x7FC0) if dtype == "bf16" else np.float32(np.nan)
+    inf_bits = np.uint16(0x7F80) if dtype == "bf16" else np.float32(np.inf)
+    bad_rows = [0, 3, wl.M - 1]
+    hidden[0, 5] = nan_bits
+    hidden[3, :] = nan_bits
+    hidden[wl.M - 1, 2] = inf_bits
+    hd, wd = to_dev(hidden, dtype, dev), to_dev(c["w_vocab"], dtype, dev)
+    td = torch.from_numpy(c["target_ids"]).to(dev)
+    say(f"slot_confidence non-finite rows {dtype}")
+    res = Z.slot_confidence(hd, wd, target_ids=td)
+    say(f"slot_sample non-finite rows {dtype}")
+    smp = Z.slot_sample(hd, wd, 0.8, seed=12, offset=3)
+    torch.cuda.synchronize()
+    hf, wf = W.as_f64(hidden, dtype), W.as_f64(c["w_vocab"], dtype)
+    ref = oracle.slot_confidence(hf, wf, target_ids=c["target_ids"])
+    sref = oracle.slot_sample(hf, wf, 0.8, 12, 3)
+    assert np.flatnonzero(ref["argmax"] < 0).tolist() == bad_rows
+    good = np.setdiff1d(np.arange(wl.M), bad_rows)
+    am = res["argmax"].cpu().numpy()
+    assert np.all(am[bad_rows] == -1), am[bad_rows]
+    for k in ("max_prob", "lse", "target_prob"):
+        assert np.all(np.isnan(res[k].cpu().numpy()[bad_rows])), k
+    sub = {k: v[good] for k, v in ref.items()}
+    check_conf({k: v[good] for k, v in res.items()}, sub, what=f"non-finite rows {dtype}, finite rows",
+               f32=dtype == "f32")
+    sid = smp["sample_id"].cpu().numpy()
+    assert np.all(sid[bad_rows] == -1), sid[bad_rows]
+    for k in ("sample_prob", "max_prob", "lse"):
+        assert np.all(np.isnan(smp[k].cpu().numpy()[bad_rows])), k
+    decided = sref["score_gap"][good] >= 1e-3 / 0.8
+    assert np.array_equal(sid[good][decided], sref["sample_id"][good][decided])
+
+
 def test_bf16_ties_take_the_lowest_id():
     dev = require_gpu()
     rng = np.random.default_rng(8)
@@ -116,14 +162,23 @@ def test_bf16_bitwise_deterministic():
 
 
 @pytest.mark.parametrize("name", ["qwen0.6b", "qwen1.7b", "qwen4b"])
-def test_full_size_sampled(name):
+def test_full_size_every_row(name):
     """Full vocabulary 151936 and full row count in the benchmark's launch
-    configuration; the oracle checks a sample of rows (all vocab entries each)."""
+    configuration: every row against the oracle (planted rows included, so
+    max_prob spans (1/V, 1))."""
     dev = require_gpu()
     wl = W.WORKLOADS[name]
-    rng = np.random.default_rng(11)
-    sample = np.unique(np.concatenate([rng.choice(wl.M, 48, replace=False), [0, wl.M - 1]]))
-    plant = _planted(wl.M, wl.vocab, 16, 3)
-    sample = np.unique(np.concatenate([sample, plant[0]]))
+    plant = _planted(wl.M, wl.vocab, 64, 3)
     say(f"slot_confidence full {name}: generating inputs")
-    _run_and_check(wl, dev, plant=plant, what=f"full {name}", sample=sample)
+    c = W.confidence_inputs(wl, plant=plant)
+    hd, wd = to_dev(c["hidden"], "bf16", dev), to_dev(c["w_vocab"], "bf16", dev)
+    td = torch.from_numpy(c["target_ids"]).to(dev)
+    say(f"slot_confidence full {name}")
+    res = Z.slot_confidence(hd, wd, target_ids=td)
+    torch.cuda.synchronize()
+    hf, wf = W.as_f64(c["hidden"], "bf16"), W.as_f64(c["w_vocab"], "bf16")
+    say(f"slot_confidence full {name}: oracle over every row")
+    ref = oracle_confidence_by_block(hf, wf, c["target_ids"])
+    check_conf(res, ref, what=f"full {name}", logit_of=lambda i, v: float(hf[i] @ wf[v]))
+    mp = res["max_prob"].cpu().numpy()
+    assert mp.max() > 0.9 and mp.min() < 1e-4

@@ -16,7 +16,7 @@ import torch
 
 import oracle
 import workloads as W
-from gpu_helpers import require_gpu, say, to_dev
+from gpu_helpers import oracle_confidence_by_block, oracle_sample_by_block, require_gpu, say, to_dev
 
 import paper_2609_19868_amd as Z
 
@@ -31,12 +31,17 @@ def _planted(M, V, n, seed):
     return rows, rng.integers(0, V, size=len(rows)), rng.uniform(0.0, 120.0, size=len(rows))
 
 
-def _check(res, hf, wf, T, seed, offset, rows, f32, what, row_ids=None):
+def _check(res, hf, wf, T, seed, offset, rows, f32, what, row_ids=None, parallel=False):
     """Compare the GPU results of `rows` with the oracle on the same rows
-    (`row_ids`: the rows' indices in the random stream, default `rows`)."""
+    (`row_ids`: the rows' indices in the random stream, default `rows`);
+    `parallel` runs the oracle on blocks of rows side by side."""
     row_ids = rows if row_ids is None else row_ids
-    ref = oracle.slot_sample(hf, wf, T, seed, offset, row_ids=row_ids)
-    conf = oracle.slot_confidence(hf, wf)
+    if parallel:
+        ref = oracle_sample_by_block(hf, wf, T, seed, offset, row_ids=row_ids)
+        conf = oracle_confidence_by_block(hf, wf)
+    else:
+        ref = oracle.slot_sample(hf, wf, T, seed, offset, row_ids=row_ids)
+        conf = oracle.slot_confidence(hf, wf)
     tol = 1e-4 if f32 else 1e-3
     sid = res["sample_id"].cpu().numpy()[rows].astype(np.int64)
     sp = res["sample_prob"].cpu().numpy().astype(np.float64)[rows]
@@ -63,7 +68,7 @@ def _check(res, hf, wf, T, seed, offset, rows, f32, what, row_ids=None):
     return int((~decided).sum()), ref, conf
 
 
-def _run(wl, dev, T, rows=None, plant=None, what="", seed=SEED, offset=OFFSET):
+def _run(wl, dev, T, rows=None, plant=None, what="", seed=SEED, offset=OFFSET, parallel=False):
     c = W.confidence_inputs(wl, plant=plant)
     hd, wd = to_dev(c["hidden"], wl.dtype, dev), to_dev(c["w_vocab"], wl.dtype, dev)
     say(f"slot_sample {what} T={T}")
@@ -72,7 +77,8 @@ def _run(wl, dev, T, rows=None, plant=None, what="", seed=SEED, offset=OFFSET):
     rows = np.arange(hd.shape[0]) if rows is None else np.asarray(rows)
     hf = W.as_f64(c["hidden"][rows], wl.dtype)
     wf = W.as_f64(c["w_vocab"], wl.dtype)
-    n_near, ref, conf = _check(res, hf, wf, T, seed, offset, rows, wl.dtype == "f32", what)
+    say(f"slot_sample {what} T={T}: oracle")
+    n_near, ref, conf = _check(res, hf, wf, T, seed, offset, rows, wl.dtype == "f32", what, parallel=parallel)
     return res, ref, conf, n_near
 
 
@@ -160,16 +166,14 @@ def test_draws_follow_the_tempered_softmax():
 
 
 @pytest.mark.parametrize("name", ["qwen0.6b", "qwen1.7b", "qwen4b"])
-def test_full_size_sampled(name):
-    """Full vocabulary and row count in the benchmark's launch configuration;
-    the oracle checks a sample of rows (every vocab entry of each)."""
+def test_full_size_every_row(name):
+    """Full vocabulary and row count in the benchmark's launch configuration:
+    every row against the oracle (every vocab entry of each)."""
     dev = require_gpu()
     wl = W.WORKLOADS[name]
-    rng = np.random.default_rng(12)
-    plant = _planted(wl.M, wl.vocab, 16, 4)
-    rows = np.unique(np.concatenate([rng.choice(wl.M, 40, replace=False), [0, wl.M - 1], plant[0]]))
+    plant = _planted(wl.M, wl.vocab, 64, 4)
     say(f"slot_sample full {name}: generating inputs")
-    _run(wl, dev, 1.0, rows=rows, plant=plant, what=f"full {name}")
+    _run(wl, dev, 1.0, plant=plant, what=f"full {name}", parallel=True)
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])

@@ -13,7 +13,8 @@ import torch
 
 import oracle
 import workloads as W
-from gpu_helpers import attn_inputs_dev, check_attn, require_gpu, say, to_dev, to_f64
+from gpu_helpers import (attn_inputs_dev, check_attn, full_attention_inputs, oracle_attention_by_row, require_gpu,
+                         say, to_dev, to_f64)
 
 import paper_2609_19868_amd as Z
 
@@ -182,46 +183,31 @@ def test_bf16_outputs_stay_inside_their_buffers():
     check_attn(to_f64(out), to_f64(lse), O, L, "bf16", "guarded")
 
 
+@pytest.mark.parametrize("pass_,pname", PASSES, ids=[p[1] for p in PASSES])
 @pytest.mark.parametrize("name", ["qwen0.6b", "qwen1.7b", "qwen4b"])
-def test_full_size_sampled(name):
-    """Full workload shapes in the launch configuration the benchmark times; the
-    oracle checks a sample of (batch, head) pairs, every token of each."""
+def test_full_size_every_head(name, pass_, pname):
+    """Full workload shapes in the launch configuration the benchmark times
+    (the library's own prefix split): every (batch, head) pair and every token
+    against the oracle, and the last token of each slot identical across the
+    two passes (it sees the same keys in both)."""
     dev = require_gpu()
     wl = W.WORKLOADS[name].replace(hidden=0, vocab=0)
-    say(f"slot_attn full {name}: generating inputs")
-    x = W.attention_inputs(wl)
-    xd = {k: to_dev(v, wl.dtype, dev) for k, v in x.items()}
-    rng = np.random.default_rng(5)
-    picks = [(int(rng.integers(wl.batch)), int(rng.integers(wl.n_q_heads))) for _ in range(3)]
-    picks.append((wl.batch - 1, wl.n_q_heads - 1))
-    G = wl.n_q_heads // wl.n_kv_heads
-    for pass_, pname in PASSES:
-        say(f"slot_attn full {name} {pname}")
-        out, lse = _run(xd, wl, pass_)
-        Og, Lg = to_f64(out), to_f64(lse)
-        for b, h in picks:
-            g = h // G
-            sub = wl.replace(batch=1, n_q_heads=1, n_kv_heads=1)
-            xf = {
-                "q": W.as_f64(x["q"][b:b + 1, h:h + 1], "bf16"),
-                "k_cache": W.as_f64(x["k_cache"][b:b + 1, g:g + 1], "bf16"),
-                "v_cache": W.as_f64(x["v_cache"][b:b + 1, g:g + 1], "bf16"),
-                "k_slot": W.as_f64(x["k_slot"][b:b + 1, g:g + 1], "bf16"),
-                "v_slot": W.as_f64(x["v_slot"][b:b + 1, g:g + 1], "bf16"),
-            }
-            O, L = _oracle(xf, sub, pass_)
-            check_attn(Og[b:b + 1, h:h + 1], Lg[b:b + 1, h:h + 1], O, L, "bf16", f"{name} {pname} b={b} h={h}")
-        # properties that hold everywhere: finite, and the last token of a slot agrees across passes
-        assert np.isfinite(Og).all() and np.isfinite(Lg).all()
-        if pass_ == Z.PASS_DIFFUSION:
-            last_diff = (Og, Lg)
-        else:
-            last = np.arange(wl.n_slots) * wl.slot_len + wl.slot_len - 1
-            assert np.abs(Og[:, :, last] - last_diff[0][:, :, last]).max() <= 1e-2
-            assert np.abs(Lg[:, :, last] - last_diff[1][:, :, last]).max() <= 1e-4
+    say(f"slot_attn full {name} {pname}: generating inputs")
+    x, xd, xf = full_attention_inputs(wl, dev)
+    say(f"slot_attn full {name} {pname}")
+    out, lse = _run(xd, wl, pass_)
+    Og, Lg = to_f64(out), to_f64(lse)
+    say(f"slot_attn full {name} {pname}: oracle over every head")
+    O, L = oracle_attention_by_row(xf, wl.prefix_len, wl.n_slots, wl.slot_len, wl.scale, pass_)
+    check_attn(Og, Lg, O, L, "bf16", f"{name} {pname}")
+    other = Z.PASS_AR_INFILL if pass_ == Z.PASS_DIFFUSION else Z.PASS_DIFFUSION
+    out2, lse2 = _run(xd, wl, other)
+    last = np.arange(wl.n_slots) * wl.slot_len + wl.slot_len - 1
+    assert np.abs(to_f64(out2)[:, :, last] - Og[:, :, last]).max() <= 1e-2
+    assert np.abs(to_f64(lse2)[:, :, last] - Lg[:, :, last]).max() <= 1e-4
 
 
-def _layout_case(wl, dev, variant, picks=None):
+def _layout_case(wl, dev, variant):
     """Training-layout attention: P = 0, every slot sees the earlier slots.
     Paper-literal reading: causal in physical order (every slot AR_INFILL).
     Variant: the masked slots (after the clean ones) are bidirectional inside."""
@@ -237,15 +223,11 @@ def _layout_case(wl, dev, variant, picks=None):
                            slot_pass=torch.from_numpy(sp).to(dev))
     torch.cuda.synchronize()
     Og, Lg = to_f64(out), to_f64(lse)
-    G = wl.n_q_heads // wl.n_kv_heads
-    pairs = picks if picks is not None else [(b, h) for b in range(wl.batch) for h in range(wl.n_q_heads)]
-    for b, h in pairs:
-        g = h // G
-        sub = wl.replace(batch=1, n_q_heads=1, n_kv_heads=1)
-        xf = {k: W.as_f64(x[k][b:b + 1, (h if k == "q" else g):(h if k == "q" else g) + 1], "bf16")
-              for k in ("q", "k_cache", "v_cache", "k_slot", "v_slot")}
-        O, L = _oracle(xf, sub, oracle.PASS_AR_INFILL, cross=oracle.CROSS_SLOT_CAUSAL, slot_pass=sp[b:b + 1])
-        check_attn(Og[b:b + 1, h:h + 1], Lg[b:b + 1, h:h + 1], O, L, "bf16", f"layout b={b} h={h} variant={variant}")
+    xf = {k: W.as_f64(v, "bf16") for k, v in x.items()}
+    say(f"layout attention N={wl.T} variant={variant}: oracle over every head")
+    O, L = oracle_attention_by_row(xf, 0, wl.n_slots, wl.slot_len, wl.scale, oracle.PASS_AR_INFILL,
+                                   cross=oracle.CROSS_SLOT_CAUSAL, slot_pass=sp)
+    check_attn(Og, Lg, O, L, "bf16", f"layout variant={variant}")
 
 
 @pytest.mark.parametrize("variant", [False, True], ids=["causal", "masked_bidirectional"])
@@ -255,7 +237,9 @@ def test_training_layout_small(variant):
     _layout_case(wl, dev, variant)
 
 
-def test_training_layout_full_size_sampled():
+def test_training_layout_full_size():
+    """The full training layout (B = 8, 16 heads, 4096 tokens), every (batch,
+    head) pair against the oracle."""
     dev = require_gpu()
     wl = W.WORKLOADS["layout"]
-    _layout_case(wl, dev, False, picks=[(0, 0), (7, 15)])
+    _layout_case(wl, dev, False)

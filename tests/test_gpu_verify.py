@@ -24,7 +24,7 @@ import paper_2609_19868_amd as Z
 pytestmark = pytest.mark.gpu
 
 
-def _selection(rng, B, S, invalid=False):
+def _selection(rng, B, S, invalid=False, repeats=False):
     sel = np.full((B, S), -1, dtype=np.int32)
     for b in range(B):
         k = int(rng.integers(0, S + 1))
@@ -33,6 +33,9 @@ def _selection(rng, B, S, invalid=False):
             sel[b, k] = S + 3  # not a slot id: skipped
             if k + 1 < S:
                 sel[b, k + 1] = int(rng.integers(0, S))  # after an invalid id the list goes on
+        if repeats and k >= 2 and rng.random() < 0.7:
+            i = int(rng.integers(1, k))
+            sel[b, i] = sel[b, int(rng.integers(0, i))]  # an earlier slot listed again: skipped
     return sel
 
 
@@ -79,7 +82,7 @@ def test_append_bit_exact(name, dtype, B, Hkv, D, C, S, L):
 
     kc, vc, ks, vs = draw((B, Hkv, C, D)), draw((B, Hkv, C, D)), draw((B, Hkv, T, D)), draw((B, Hkv, T, D))
     acc = (rng.random((B, S, L)) < 0.6).astype(np.uint8)
-    order = _selection(rng, B, S, invalid=True)
+    order = _selection(rng, B, S, invalid=True, repeats=True)
     plens = rng.integers(0, max(1, C - T), B).astype(np.int32)
     plens[0] = C - 1 if B > 1 else plens[0]  # cannot fit unless nothing is appended
     if B > 2:
