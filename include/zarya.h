@@ -211,6 +211,24 @@ zarya_status zarya_slot_confidence(const zarya_conf_desc* desc, const void* hidd
                                    float* lse, float* target_prob, void* workspace,
                                    size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * zarya_slot_confidence without a workspace, for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc.  Same arguments and results as
+ * zarya_slot_confidence (bit-identical); the partials live in a static device
+ * array of the library, 1 MiB per GPU (loaded with the library's code, held
+ * until the process ends), whose address is looked up on the first call on
+ * each device.  Every bf16 call with n_rows <= 65536 fits; a call whose
+ * partials need more returns ZARYA_ERR_UNSUPPORTED before anything is
+ * launched.  All calls on one GPU share that array: calls that overlap on one
+ * GPU (different streams without ordering, or different host threads) race
+ * and give wrong results; calls ordered on one stream are safe.  Nothing in
+ * the array needs to start at any value.  No device memory is allocated.
+ */
+zarya_status zarya_slot_confidence_noalloc(const zarya_conf_desc* desc, const void* hidden, const void* w_vocab,
+                                           const int32_t* target_ids, float* max_prob, int32_t* argmax_id,
+                                           float* lse, float* target_prob, hipStream_t stream);
+
 /* ------------------------------------------------------------------------ */
 /* 3. First-hitting slot selection                                           */
 /* ------------------------------------------------------------------------ */

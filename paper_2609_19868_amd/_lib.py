@@ -43,6 +43,7 @@ EXPORTS = (
     "zarya_slot_attn",
     "zarya_slot_confidence_workspace_size",
     "zarya_slot_confidence",
+    "zarya_slot_confidence_noalloc",
     "zarya_select_slots",
     "zarya_verify_accept",
     "zarya_kv_append",
@@ -142,6 +143,8 @@ def lib():
         L.zarya_slot_confidence_workspace_size.restype = ctypes.c_int
         L.zarya_slot_confidence.argtypes = [ctypes.POINTER(ConfDesc), vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         L.zarya_slot_confidence.restype = ctypes.c_int
+        L.zarya_slot_confidence_noalloc.argtypes = [ctypes.POINTER(ConfDesc), vp, vp, vp, vp, vp, vp, vp, vp]
+        L.zarya_slot_confidence_noalloc.restype = ctypes.c_int
         L.zarya_select_slots.argtypes = [i32, i32, i32, vp, vp, i32, i32, f32, i32, vp, vp, vp, vp]
         L.zarya_select_slots.restype = ctypes.c_int
         L.zarya_verify_accept.argtypes = [i32, i32, i32, vp, vp, f32, i32, vp, vp, vp, vp]

@@ -7,12 +7,19 @@
 
 #include <algorithm>
 #include <cmath>
+#include <mutex>
 #include <string>
 
 #include "kernels.hpp"
 #include "zarya.h"
 
 using namespace zarya;
+
+// Partials of zarya_slot_confidence_noalloc.  Every GPU the library runs on
+// holds its own copy (allocated when the code object is loaded, kept until
+// the process ends).  In host code this name is a host-side stand-in, not a
+// device address: the device address comes from hipGetSymbolAddress.
+static __device__ __align__(256) uint8_t scratch[kConfScratchBytes];
 
 namespace {
 
@@ -181,6 +188,29 @@ ConfPlan plan_conf(const zarya_conf_desc* d) {
 size_t sample_ws_bytes(const zarya_conf_desc* d) {
   const ConfPlan pl = plan_conf(d);
   return pl.ws_bytes + 2 * align256((size_t)pl.n_vg * d->n_rows * 4);
+}
+
+// Device address of `scratch` on the current device, looked up once per
+// device (with that device current) and kept.
+constexpr int kMaxDevices = 256;
+void* g_scratch_addr[kMaxDevices];
+std::mutex g_scratch_mutex;
+
+zarya_status current_device_scratch(void** addr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_status(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(ZARYA_ERR_UNSUPPORTED, "device index %d", dev);
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_status(e, "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(ZARYA_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_addr[dev] = p;
+  }
+  *addr = g_scratch_addr[dev];
+  return ZARYA_OK;
 }
 
 // Enqueues the LM-head reduction and its merge; with `sp` also the sampling.
@@ -397,6 +427,24 @@ zarya_status zarya_slot_confidence(const zarya_conf_desc* d, const void* hidden,
   if (!workspace) return fail(ZARYA_ERR_INVALID_ARGUMENT, "workspace is NULL");
   return run_conf(d, nullptr, hidden, nullptr, d->n_rows, w_vocab, target_ids, max_prob, argmax_id, lse, target_prob,
                   nullptr, nullptr, workspace, stream);
+}
+
+zarya_status zarya_slot_confidence_noalloc(const zarya_conf_desc* d, const void* hidden, const void* w_vocab,
+                                           const int32_t* target_ids, float* max_prob, int32_t* argmax_id,
+                                           float* lse, float* target_prob, hipStream_t stream) {
+  zarya_status st = check_conf_desc(d);
+  if (st != ZARYA_OK) return st;
+  if (!hidden || !w_vocab || !max_prob || !argmax_id)
+    return fail(ZARYA_ERR_INVALID_ARGUMENT, "hidden, w_vocab, max_prob and argmax_id are required");
+  const ConfPlan pl = plan_conf(d);
+  if (pl.ws_bytes > kConfScratchBytes)
+    return fail(ZARYA_ERR_UNSUPPORTED, "the partials of this call need %zu bytes; the library's scratch holds %zu",
+                pl.ws_bytes, kConfScratchBytes);
+  void* ws = nullptr;
+  st = current_device_scratch(&ws);
+  if (st != ZARYA_OK) return st;
+  return run_conf(d, nullptr, hidden, nullptr, d->n_rows, w_vocab, target_ids, max_prob, argmax_id, lse, target_prob,
+                  nullptr, nullptr, ws, stream);
 }
 
 zarya_status zarya_slot_sample_workspace_size(const zarya_conf_desc* desc, size_t* bytes) {

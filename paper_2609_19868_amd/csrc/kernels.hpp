@@ -169,6 +169,10 @@ constexpr int kAttnWideRowsPerBlock = 256;  // eight waves: every K/V tile stage
 constexpr int kConfNW = 8, kConfBR = 256, kConfBK = 64, kConfNSW = 3, kConfNSX = 2;
 constexpr int kConfSmallNW = 4, kConfSmallBR = 64, kConfSmallMaxRows = 128;
 constexpr int kConfTargetWGs = 256;
+// Device scratch of zarya_slot_confidence_noalloc: room for the partials of
+// every bf16 call up to 65536 rows (row tiles x vocabulary groups <= 256, 12
+// bytes per row and group).
+constexpr size_t kConfScratchBytes = (size_t)1 << 20;
 constexpr int conf_tile_rows(int n_rows) { return n_rows <= kConfSmallMaxRows ? kConfSmallBR : kConfBR; }
 
 hipError_t launch_slot_attn_bf16(const AttnParams& p, int head_dim, hipStream_t stream);

@@ -114,6 +114,25 @@ def test_slot_attn_plan_reports_the_decomposition():
     assert _lib.lib().zarya_slot_attn_plan(ctypes.byref(d), None) == _lib.ERR_INVALID_ARGUMENT
 
 
+def test_noalloc_confidence_rejects_before_touching_a_device():
+    """The allocation-free confidence call validates its descriptor and the
+    size of its partials first: on this host, without a GPU, a bad or
+    oversized call returns its status without reaching the runtime."""
+    L = _lib.lib()
+    d = _lib.ConfDesc(n_rows=0, hidden=64, vocab=100, dtype=_lib.DTYPE_BF16)
+    p = ctypes.c_void_p(16)
+    assert L.zarya_slot_confidence_noalloc(ctypes.byref(d), p, p, None, p, p, None, None, None) == \
+        _lib.ERR_INVALID_ARGUMENT
+    d = _lib.ConfDesc(n_rows=8, hidden=64, vocab=100, dtype=_lib.DTYPE_BF16)
+    assert L.zarya_slot_confidence_noalloc(ctypes.byref(d), p, None, None, p, p, None, None, None) == \
+        _lib.ERR_INVALID_ARGUMENT
+    # float32, 1400 rows x 64 vocabulary groups of 12-byte partials: more than the 1 MiB scratch
+    d = _lib.ConfDesc(n_rows=1400, hidden=8, vocab=131072, dtype=_lib.DTYPE_F32)
+    assert L.zarya_slot_confidence_noalloc(ctypes.byref(d), p, p, None, p, p, None, None, None) == \
+        _lib.ERR_UNSUPPORTED
+    assert b"scratch" in L.zarya_last_error()
+
+
 def test_slot_attn_workspace_sizes():
     # one split needs no workspace; several splits need fp32 partials of O and LSE
     d1 = _desc(prefix_splits=1)
