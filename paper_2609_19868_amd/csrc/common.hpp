@@ -124,6 +124,22 @@ __device__ __forceinline__ float max3f(float a, float b, float c) {
   return r;
 }
 
+// max(x, x of lane ^ 32) on every lane, through v_permlane32_swap (a VALU
+// exchange of the two 32-lane halves; no LDS round trip).  The swap leaves
+// each lane holding its own value in one output and its partner's in the
+// other, so the maximum of the two outputs is the pair's maximum.
+__device__ __forceinline__ float max_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return max3f(__uint_as_float(r[0]), __uint_as_float(r[1]), __uint_as_float(r[1]));
+}
+
+// x + x of lane ^ 32 on every lane (the same value on both lanes of a pair:
+// float addition is commutative).
+__device__ __forceinline__ float sum_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC 2011): four 32-bit words from
 // a 128-bit counter and a 64-bit key.  Each round multiplies counter words 0
 // and 2 by the two round constants, swaps the halves of the products into the

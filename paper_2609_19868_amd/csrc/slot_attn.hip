@@ -43,14 +43,17 @@ constexpr int KT = 64;          // keys per tile
 constexpr float kRescaleLog2 = 8.f;  // growth of a row maximum (log2 units) that forces a rescale
 
 // XOR swizzle of the 16-byte chunk index of LDS row `kr` (D = 128: 16 chunks
-// per row; D = 64: 8).  Keeps the 32 rows of one K-fragment read and the 4
-// rows of one transposing V read on distinct banks.
+// per row; D = 64: 8).  Any 16 consecutive rows (the rows one pass of a
+// K-fragment ds_read_b128 serves) get distinct bank groups, and the aligned
+// chunk pairs of 4 consecutive rows (one transposing V read) stay aligned
+// pairs on distinct banks: the pair index takes the low row bits, the chunk's
+// low bit the next one.
 template <int D>
 __device__ __forceinline__ int swz(int kr) {
   if constexpr (D == 128) {
-    return (kr & 7) << 1;
+    return ((kr & 7) << 1) | ((kr >> 3) & 1);
   } else {
-    return ((kr >> 1) & 3) << 1;
+    return (((kr >> 1) & 3) << 1) | ((kr >> 3) & 1);
   }
 }
 
@@ -199,11 +202,14 @@ __global__ __launch_bounds__(NWAVE * 64) __attribute__((amdgpu_waves_per_eu(ZARY
   for (int ks = 0; ks < NKS; ++ks) k_col[ks] = n * ROWB + (((2 * ks + hh) ^ swz<D>(n)) << 4);
   const int q16 = lane >> 4, rr = lane & 15;
   const int vrow = 4 * hh + (rr >> 2);  // first key row of this lane's transposing reads (+16*st, +8)
-  uint32_t v_col[NDB];
+  // (rows vrow + 16 * step and vrow + 8 + 16 * step: the swizzle repeats every
+  // 16 rows, so the two halves of a step have addresses of their own)
+  uint32_t v_col[NDB], v_col8[NDB];
 #pragma unroll
   for (int db = 0; db < NDB; ++db) {
     const int d = db * 32 + (q16 & 1) * 16 + 4 * (rr & 3);
     v_col[db] = vrow * ROWB + (((d >> 3) ^ swz<D>(vrow)) << 4) + (d & 7) * 2;
+    v_col8[db] = (vrow + 8) * ROWB + (((d >> 3) ^ swz<D>(vrow + 8)) << 4) + (d & 7) * 2;
   }
 
   for (int st = 0; st < NS - 1 && st < nt; ++st) issue(st, st);
@@ -236,7 +242,8 @@ __global__ __launch_bounds__(NWAVE * 64) __attribute__((amdgpu_waves_per_eu(ZARY
 
     // ---- S^T = K Q^T for two 32-key blocks; register v of block kb holds
     // key kb*32 + 8*(v/4) + 4*hh + v%4 of the tile.  K fragments are read
-    // one k-step ahead of their MFMAs.
+    // one k-step ahead of their MFMAs (deeper read-ahead measured no faster:
+    // the other wave of the SIMD covers the LDS latency).
     f32x16 sacc[2] = {f32x16{}, f32x16{}};
     {
       bf16x8 kf[2][2];
@@ -264,7 +271,7 @@ __global__ __launch_bounds__(NWAVE * 64) __attribute__((amdgpu_waves_per_eu(ZARY
 #pragma unroll
     for (int db = 0; db < NDB; ++db) {
       vf[0][db][0] = lds_read_tr16_b64<0>(vb_addr + v_col[db]);
-      vf[0][db][1] = lds_read_tr16_b64<8 * ROWB>(vb_addr + v_col[db]);
+      vf[0][db][1] = lds_read_tr16_b64<0>(vb_addr + v_col8[db]);
     }
 
     // ---- online softmax; masks only on tiles that need them
@@ -282,13 +289,21 @@ __global__ __launch_bounds__(NWAVE * 64) __attribute__((amdgpu_waves_per_eu(ZARY
           if ((unsigned)(key - lim_lo) >= (unsigned)lim_n) sacc[kb][v] = -INFINITY;
         }
     }
-    float mt = max3f(sacc[0][0], sacc[0][1], sacc[1][0]);
+    // tile maximum of this lane's row: a max3 tree (depth 3 instead of a
+    // 16-long chain), then the other lane half of the row
+    float mt;
+    {
+      float t[11];
 #pragma unroll
-    for (int v = 2; v < 16; v += 2) mt = max3f(mt, sacc[0][v], sacc[0][v + 1]);
+      for (int j = 0; j < 5; ++j) t[j] = max3f(sacc[0][3 * j], sacc[0][3 * j + 1], sacc[0][3 * j + 2]);
+      t[5] = max3f(sacc[0][15], sacc[1][0], sacc[1][1]);
 #pragma unroll
-    for (int v = 1; v < 15; v += 2) mt = max3f(mt, sacc[1][v], sacc[1][v + 1]);
-    mt = max3f(mt, sacc[1][15], sacc[1][15]);
-    mt = fmaxf(mt, __shfl_xor(mt, 32));
+      for (int j = 0; j < 4; ++j) t[6 + j] = max3f(sacc[1][3 * j + 2], sacc[1][3 * j + 3], sacc[1][3 * j + 4]);
+      t[10] = max3f(sacc[1][14], sacc[1][15], sacc[1][15]);
+      const float u0 = max3f(t[0], t[1], t[2]), u1 = max3f(t[3], t[4], t[5]);
+      const float u2 = max3f(t[6], t[7], t[8]), u3 = max3f(t[9], t[10], t[10]);
+      mt = max_xor32(max3f(max3f(u0, u1, u2), u3, u3));
+    }
     const float m_new = fmaxf(m_run, mt);
     // Rescale only when the maximum of some row moved by more than 2^8 in
     // probability: until then the exponentials below are taken against the
@@ -336,7 +351,7 @@ __global__ __launch_bounds__(NWAVE * 64) __attribute__((amdgpu_waves_per_eu(ZARY
 #pragma unroll
         for (int db = 0; db < NDB; ++db) {
           vf[sl ^ 1][db][0] = lds_read_tr16_b64<0>(vb_addr + v_col[db] + 16 * (stp + 1) * ROWB);
-          vf[sl ^ 1][db][1] = lds_read_tr16_b64<8 * ROWB>(vb_addr + v_col[db] + 16 * (stp + 1) * ROWB);
+          vf[sl ^ 1][db][1] = lds_read_tr16_b64<0>(vb_addr + v_col8[db] + 16 * (stp + 1) * ROWB);
         }
         lds_wait<2 * NDB>();
       } else {
@@ -355,7 +370,7 @@ __global__ __launch_bounds__(NWAVE * 64) __attribute__((amdgpu_waves_per_eu(ZARY
   }
 
   // ---- finalize: combine the two lane halves' partial sums
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  const float l_tot = sum_xor32(l_run);
   if (!row_ok) return;
   const size_t grow = (size_t)bg * p.R + row;  // row of the [B*Hq*T] output
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
