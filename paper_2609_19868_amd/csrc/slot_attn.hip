@@ -49,7 +49,7 @@ constexpr float kRescaleLog2 = 8.f;  // growth of a row maximum (log2 units) tha
 // pairs on distinct banks: the pair index takes the low row bits, the chunk's
 // low bit the next one.
 template <int D>
-__device__ __forceinline__ int swz(int kr) {
+__host__ __device__ constexpr int swz(int kr) {
   if constexpr (D == 128) {
     return ((kr & 7) << 1) | ((kr >> 3) & 1);
   } else {
@@ -197,84 +197,68 @@ __global__ __launch_bounds__(NWAVE * 64) __attribute__((amdgpu_waves_per_eu(ZARY
   // lane-dependent parts of the LDS fragment addresses (the swizzle of every
   // row a lane reads depends on the lane only)
   const uint32_t lds0 = lds_addr(&lds[0][0][0]);
-  uint32_t k_col[NKS];
-#pragma unroll
-  for (int ks = 0; ks < NKS; ++ks) k_col[ks] = n * ROWB + (((2 * ks + hh) ^ swz<D>(n)) << 4);
+  // K fragment of k-step ks: row n, logical chunk 2*ks + hh, i.e. physical
+  // chunk (2*ks) ^ (hh ^ swz(n)) (2*ks is even, hh the low bit)
+  const uint32_t k_row = n * ROWB;
+  const uint32_t k_cx = (uint32_t)((hh ^ swz<D>(n)) << 4);
+  auto k_col = [&](int ks) { return k_row + (k_cx ^ ((uint32_t)ks << 5)); };
   const int q16 = lane >> 4, rr = lane & 15;
   const int vrow = 4 * hh + (rr >> 2);  // first key row of this lane's transposing reads (+16*st, +8)
-  // (rows vrow + 16 * step and vrow + 8 + 16 * step: the swizzle repeats every
-  // 16 rows, so the two halves of a step have addresses of their own)
-  uint32_t v_col[NDB], v_col8[NDB];
+  // Rows vrow + 16 * step and vrow + 8 + 16 * step: the swizzle repeats every
+  // 16 rows and, for vrow < 8, swz(vrow + 8) = swz(vrow) ^ 1, which flips bit
+  // 4 of the address (the chunk's low bit): the second half of a step is read
+  // at (v_col ^ 16) + 8 rows.
+  uint32_t v_col[NDB];
 #pragma unroll
   for (int db = 0; db < NDB; ++db) {
     const int d = db * 32 + (q16 & 1) * 16 + 4 * (rr & 3);
     v_col[db] = vrow * ROWB + (((d >> 3) ^ swz<D>(vrow)) << 4) + (d & 7) * 2;
-    v_col8[db] = (vrow + 8) * ROWB + (((d >> 3) ^ swz<D>(vrow + 8)) << 4) + (d & 7) * 2;
   }
+  static_assert((swz<D>(8) ^ swz<D>(0)) == 1, "second V half-step addressing assumes swz(r + 8) = swz(r) ^ 1");
 
-  for (int st = 0; st < NS - 1 && st < nt; ++st) issue(st, st);
+  f32x16 sacc[2];   // scores of the tile between its QK^T and its softmax
+  bf16x8 pb[4];      // its probabilities (bf16, B operands of the PV steps)
+  v4i16 vf[2][NDB][2];  // V^T fragments, double-buffered across PV steps
 
-  for (int i = 0; i < nt; ++i) {
-    const int buf = i % NS;
-    const int ahead = min(nt - 1, i + NS - 2) - i;  // later tiles whose loads may still fly
-    if constexpr (NS >= 4) {
-      if (ahead >= 2) {
-        wait_vmcnt<2 * LPT>();
-      } else if (ahead == 1) {
-        wait_vmcnt<LPT>();
-      } else {
-        wait_vmcnt<0>();
-      }
-    } else if constexpr (NS == 3) {
-      if (ahead >= 1) {
-        wait_vmcnt<LPT>();
-      } else {
-        wait_vmcnt<0>();
-      }
-    } else {
-      wait_vmcnt<0>();
-    }
-    block_barrier();
-    if (i + NS - 1 < nt) issue(i + NS - 1, (i + NS - 1) % NS);
-
-    const uint32_t kb_addr = lds0 + buf * (2 * TILEB);
-    const uint32_t vb_addr = kb_addr + TILEB;
-
-    // ---- S^T = K Q^T for two 32-key blocks; register v of block kb holds
-    // key kb*32 + 8*(v/4) + 4*hh + v%4 of the tile.  K fragments are read
-    // one k-step ahead of their MFMAs (deeper read-ahead measured no faster:
-    // the other wave of the SIMD covers the LDS latency).
-    f32x16 sacc[2] = {f32x16{}, f32x16{}};
-    {
-      bf16x8 kf[2][2];
-      kf[0][0] = lds_read_b128<0>(kb_addr + k_col[0]);
-      kf[0][1] = lds_read_b128<32 * ROWB>(kb_addr + k_col[0]);
+  // ---- S^T = K Q^T of tile i for two 32-key blocks; register v of block kb
+  // holds key kb*32 + 8*(v/4) + 4*hh + v%4 of the tile.  K fragments are read
+  // one k-step ahead of their MFMAs (deeper read-ahead measured no faster).
+  auto qk = [&](int i) {
+    const uint32_t kb_addr = lds0 + (i % NS) * (2 * TILEB);
+    sacc[0] = f32x16{};
+    sacc[1] = f32x16{};
+    bf16x8 kf[2][2];
+    kf[0][0] = lds_read_b128<0>(kb_addr + k_col(0));
+    kf[0][1] = lds_read_b128<32 * ROWB>(kb_addr + k_col(0));
 #pragma unroll
-      for (int ks = 0; ks < NKS; ++ks) {
-        const int sl = ks & 1;
-        if (ks + 1 < NKS) {
-          kf[sl ^ 1][0] = lds_read_b128<0>(kb_addr + k_col[ks + 1]);
-          kf[sl ^ 1][1] = lds_read_b128<32 * ROWB>(kb_addr + k_col[ks + 1]);
-          lds_wait<2>();
-        } else {
-          lds_wait<0>();
-        }
-        lds_tie(kf[sl][0]);
-        lds_tie(kf[sl][1]);
-        sacc[0] = mfma32x32x16(kf[sl][0], qf[ks], sacc[0]);
-        sacc[1] = mfma32x32x16(kf[sl][1], qf[ks], sacc[1]);
+    for (int ks = 0; ks < NKS; ++ks) {
+      const int sl = ks & 1;
+      if (ks + 1 < NKS) {
+        kf[sl ^ 1][0] = lds_read_b128<0>(kb_addr + k_col(ks + 1));
+        kf[sl ^ 1][1] = lds_read_b128<32 * ROWB>(kb_addr + k_col(ks + 1));
+        lds_wait<2>();
+      } else {
+        lds_wait<0>();
       }
+      lds_tie(kf[sl][0]);
+      lds_tie(kf[sl][1]);
+      sacc[0] = mfma32x32x16(kf[sl][0], qf[ks], sacc[0]);
+      sacc[1] = mfma32x32x16(kf[sl][1], qf[ks], sacc[1]);
     }
+  };
 
-    // ---- V^T fragments of the first PV step, issued before the softmax
-    v4i16 vf[2][NDB][2];
+  // ---- V^T fragments of the first PV step of tile i
+  auto pv_start = [&](int i) {
+    const uint32_t vb_addr = lds0 + (i % NS) * (2 * TILEB) + TILEB;
 #pragma unroll
     for (int db = 0; db < NDB; ++db) {
       vf[0][db][0] = lds_read_tr16_b64<0>(vb_addr + v_col[db]);
-      vf[0][db][1] = lds_read_tr16_b64<0>(vb_addr + v_col8[db]);
+      vf[0][db][1] = lds_read_tr16_b64<8 * ROWB>(vb_addr + (v_col[db] ^ 16u));
     }
+  };
 
-    // ---- online softmax; masks only on tiles that need them
+  // ---- online softmax of tile i's scores; masks only on tiles that need them
+  auto softmax = [&](int i) {
     const bool is_slot = i >= n_pre;
     const int key0 = is_slot ? slot_lo + (i - n_pre) * KT : (pre_begin + i) * KT;
     const bool full = !is_slot && key0 + KT <= Pb;
@@ -310,7 +294,8 @@ __global__ __launch_bounds__(NWAVE * 64) __attribute__((amdgpu_waves_per_eu(ZARY
     // stale maximum and stay <= 2^8 (exact in the float32 sums, same relative
     // rounding in bf16), and the final O / l and LSE do not depend on which
     // maximum was used.  Random scores raise a row's maximum on most early
-    // tiles, each time by little; this skips those rescales.
+    // tiles, each time by little; this skips those rescales.  Every PV of the
+    // earlier tiles is in oacc before this (the callers keep that order).
     if (__any((m_new - m_run) * c2 > kRescaleLog2)) {
       const float alpha = fast_exp2((m_run - m_new) * c2);
       l_run *= alpha;
@@ -322,7 +307,6 @@ __global__ __launch_bounds__(NWAVE * 64) __attribute__((amdgpu_waves_per_eu(ZARY
     }
     const float mc = m_run * c2;
     float ps[4] = {0.f, 0.f, 0.f, 0.f};
-    bf16x8 pb[4];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -340,10 +324,13 @@ __global__ __launch_bounds__(NWAVE * 64) __attribute__((amdgpu_waves_per_eu(ZARY
         pb[2 * kb + half] = __builtin_bit_cast(bf16x8, make_uint4(pk[0], pk[1], pk[2], pk[3]));
       }
     l_run += (ps[0] + ps[1]) + (ps[2] + ps[3]);
+  };
 
-    // ---- O^T += V^T P^T.  Step st covers keys 16*st + 4*hh + {0..3} (slots
-    // 0-3) and 16*st + 8 + 4*hh + {0..3} (slots 4-7); V^T fragments are read
-    // one step ahead with the transposing LDS read.
+  // ---- O^T += V^T P^T of tile i (after pv_start(i)).  Step st covers keys
+  // 16*st + 4*hh + {0..3} (slots 0-3) and 16*st + 8 + 4*hh + {0..3} (slots
+  // 4-7); V^T fragments are read one step ahead with the transposing LDS read.
+  auto pv_finish = [&](int i) {
+    const uint32_t vb_addr = lds0 + (i % NS) * (2 * TILEB) + TILEB;
 #pragma unroll
     for (int stp = 0; stp < 4; ++stp) {
       const int sl = stp & 1;
@@ -351,7 +338,7 @@ __global__ __launch_bounds__(NWAVE * 64) __attribute__((amdgpu_waves_per_eu(ZARY
 #pragma unroll
         for (int db = 0; db < NDB; ++db) {
           vf[sl ^ 1][db][0] = lds_read_tr16_b64<0>(vb_addr + v_col[db] + 16 * (stp + 1) * ROWB);
-          vf[sl ^ 1][db][1] = lds_read_tr16_b64<0>(vb_addr + v_col8[db] + 16 * (stp + 1) * ROWB);
+          vf[sl ^ 1][db][1] = lds_read_tr16_b64<8 * ROWB>(vb_addr + (v_col[db] ^ 16u) + 16 * (stp + 1) * ROWB);
         }
         lds_wait<2 * NDB>();
       } else {
@@ -367,6 +354,34 @@ __global__ __launch_bounds__(NWAVE * 64) __attribute__((amdgpu_waves_per_eu(ZARY
         oacc[db] = mfma32x32x16(a, pb[stp], oacc[db]);
       }
     }
+  };
+
+  for (int st = 0; st < NS - 1 && st < nt; ++st) issue(st, st);
+  for (int i = 0; i < nt; ++i) {
+    const int ahead = min(nt - 1, i + NS - 2) - i;  // later tiles whose loads may still fly
+    if constexpr (NS >= 4) {
+      if (ahead >= 2) {
+        wait_vmcnt<2 * LPT>();
+      } else if (ahead == 1) {
+        wait_vmcnt<LPT>();
+      } else {
+        wait_vmcnt<0>();
+      }
+    } else if constexpr (NS == 3) {
+      if (ahead >= 1) {
+        wait_vmcnt<LPT>();
+      } else {
+        wait_vmcnt<0>();
+      }
+    } else {
+      wait_vmcnt<0>();
+    }
+    block_barrier();
+    if (i + NS - 1 < nt) issue(i + NS - 1, (i + NS - 1) % NS);
+    qk(i);
+    pv_start(i);  // in flight during the softmax
+    softmax(i);
+    pv_finish(i);
   }
 
   // ---- finalize: combine the two lane halves' partial sums
