@@ -162,6 +162,27 @@ __host__ __device__ __forceinline__ uint4 philox4x32_10(uint32_t c0, uint32_t c1
   return make_uint4(c0, c1, c2, c3);
 }
 
+// The same generator for device code on gfx950: each round's two
+// three-operand XORs (product half ^ counter word ^ key) are one v_bitop3_b32
+// each (truth table 0x96 = a ^ b ^ c).  Bit-identical to philox4x32_10.
+__device__ __forceinline__ uint4 philox4x32_10_dev(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3, uint32_t k0,
+                                                   uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    const uint64_t p0 = (uint64_t)0xD2511F53u * c0;
+    const uint64_t p1 = (uint64_t)0xCD9E8D57u * c2;
+    const uint32_t n0 = __builtin_amdgcn_bitop3_b32((uint32_t)(p1 >> 32), c1, k0, 0x96);
+    const uint32_t n2 = __builtin_amdgcn_bitop3_b32((uint32_t)(p0 >> 32), c3, k1, 0x96);
+    c1 = (uint32_t)p1;
+    c3 = (uint32_t)p0;
+    c0 = n0;
+    c2 = n2;
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+  return make_uint4(c0, c1, c2, c3);
+}
+
 // Gumbel part of a perturbed score in the log2 domain: -log2(-log2 u) with
 // u = ((x >> 9) + 1/2) * 2^-23 in (0, 1), exact in float32.  Adding it to
 // z * log2(e) / T gives log2(e) * (z / T + G) up to a constant, G standard

@@ -37,7 +37,7 @@ __device__ __forceinline__ uint32_t conf_desc_key(float c) {
 // Philox uniform of (row, position) as its 23-bit integer (x >> 9): the same
 // order as u = ((x >> 9) + 1/2) * 2^-23.
 __device__ __forceinline__ uint32_t uniform_bits(const RevealParams& p, int row, int pos) {
-  const uint4 r = philox4x32_10((uint32_t)pos >> 2, (uint32_t)row, p.off_lo, p.off_hi, p.seed_lo, p.seed_hi);
+  const uint4 r = philox4x32_10_dev((uint32_t)pos >> 2, (uint32_t)row, p.off_lo, p.off_hi, p.seed_lo, p.seed_hi);
   const uint32_t w[4] = {r.x, r.y, r.z, r.w};
   return w[pos & 3] >> 9;
 }

@@ -166,7 +166,7 @@ __device__ __forceinline__ void sample_fold(const f32x16 (&acc)[4][JB], int lim,
       const int c0 = ib * 32 + 8 * q;  // offsets c0 .. c0+3 hold ids id0 + c0 .. + 3
 #pragma unroll
       for (int jb = 0; jb < JB; ++jb) {
-        const uint4 r = philox4x32_10((uint32_t)(id0 + c0) >> 2, (uint32_t)(row + 32 * jb), p.off_lo, p.off_hi,
+        const uint4 r = philox4x32_10_dev((uint32_t)(id0 + c0) >> 2, (uint32_t)(row + 32 * jb), p.off_lo, p.off_hi,
                                       p.seed_lo, p.seed_hi);
         const uint32_t words[4] = {r.x, r.y, r.z, r.w};
 #pragma unroll
@@ -527,7 +527,7 @@ __global__ __launch_bounds__(256) void slot_conf_f32_kernel(ConfParams p) {
     float z = 0.f;
     for (int k = 0; k < p.H; ++k) z = fmaf(hs[k], wr[k], z);
     if (p.part_g) {
-      const uint4 r = philox4x32_10((uint32_t)v >> 2, (uint32_t)row, p.off_lo, p.off_hi, p.seed_lo, p.seed_hi);
+      const uint4 r = philox4x32_10_dev((uint32_t)v >> 2, (uint32_t)row, p.off_lo, p.off_hi, p.seed_lo, p.seed_hi);
       const uint32_t words[4] = {r.x, r.y, r.z, r.w};
       const float sc = fmaf(z, p.c2t, gumbel_log2(words[v & 3]));
       if (sc > g) {
