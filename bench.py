@@ -18,8 +18,10 @@ P=4096, S=16, L=4, H=2048; top-4 slots by mean max-prob) steps under
 rotated so that neither the KV cache nor the LM head is served from the
 256 MB Infinity Cache.
 
-Times come from HIP events recorded on the stream the library launches on
-(torch's current stream); `roofline` is the dominant kernel's
+Every measurement first runs its own work back to back, untimed, for
+--spin-up seconds (the GPU clock settles after idle gaps), then its warm-up
+steps, then the timed steps.  Times come from HIP events recorded on the
+stream the library launches on (torch's current stream); `roofline` is the dominant kernel's
 (slot_confidence, against the bf16 MFMA peak) and `roofline_slot_attn` the
 attention's, against both the HBM and the MFMA peak.  The float64 CPU oracle
 is timed on the host cores as a reference baseline.
@@ -29,6 +31,7 @@ from __future__ import annotations
 
 import argparse
 import hashlib
+import itertools
 import json
 import os
 import re
@@ -54,6 +57,27 @@ SELECTION = {
 # which peak bounds the attention of each workload (algorithmic flops / bytes against the ridge point)
 ATTN_BOUND = {"qwen0.6b": "hbm", "qwen1.7b": "hbm", "qwen4b": "mfma"}
 COUNTERS = os.path.join(ROOT, "profiles", "hbm_traffic_{}.md")
+# Seconds of untimed back-to-back work before each measurement's warm-up steps
+# (--spin-up).  After an idle gap (input generation, the CPU oracle) the GPU
+# clock needs tens of milliseconds of load to settle: at qwen4b the first 10
+# steps after 3 s idle averaged 1.46 ms, the next three blocks of 10
+# 1.06 / 1.02 / 1.01 ms, and every later block 0.98-0.99 ms.
+SPIN_UP_S = 0.25
+
+
+def spin_up(fn, seconds):
+    """Call fn() back to back until `seconds` of wall time have passed (the
+    device is synchronised every 8 calls); returns the number of calls."""
+    import torch
+
+    n = 0
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(8):
+            fn()
+        n += 8
+        torch.cuda.synchronize()
+    return n
 
 
 def quantile(sorted_vals, q):
@@ -153,7 +177,7 @@ def attn_work(wl):
     return nbytes, flops
 
 
-def measure_workload(name, steps, warmup, extras, want_cpu):
+def measure_workload(name, steps, warmup, extras, want_cpu, spin_s=SPIN_UP_S):
     """Time the scoring step of one workload; returns its record (and runs the
     extras that belong to it)."""
     import numpy as np
@@ -215,6 +239,8 @@ def measure_workload(name, steps, warmup, extras, want_cpu):
             evs[3].record()
 
     def timed(pass_, K, Wm):
+        ctr = itertools.count()
+        spin_up(lambda: step(sets[next(ctr) % n_sets], pass_), spin_s)
         for i in range(Wm):
             step(sets[i % n_sets], pass_)
         torch.cuda.synchronize()
@@ -278,25 +304,25 @@ def measure_workload(name, steps, warmup, extras, want_cpu):
     }
     if "graph" in extras:
         log(f"{name}: timing the same step replayed from HIP graphs")
-        rec["graph_step"] = graph_step(step, sets, steps)
+        rec["graph_step"] = graph_step(step, sets, steps, spin_s)
     if "ar_infill" in extras:
         log(f"{name}: timing the AR_INFILL (verification) pass")
         ms_ar, mean_ar, _, _ = timed(Z.PASS_AR_INFILL, max(10, steps // 2), 3)
         rec["ar_infill_pass"] = {"steps_per_s": 1e3 / ms_ar, "slot_attn_us": mean_ar[0] * 1e3}
     if "verification" in extras:
         log(f"{name}: timing the verification step")
-        rec["verification_step"] = verification_step(dev, wl, sets[0], conf_out, sel_out, max(10, steps // 2))
+        rec["verification_step"] = verification_step(dev, wl, sets[0], conf_out, sel_out, max(10, steps // 2), spin_s)
     if "sampled" in extras:
         log(f"{name}: timing the sampled LM-head reduction (Gumbel-max, T = 1)")
-        rec["sampled_draft"] = sampled_draft(dev, wl, sets, max(10, steps // 2), conf_ms)
+        rec["sampled_draft"] = sampled_draft(dev, wl, sets, max(10, steps // 2), conf_ms, spin_s)
     if "mode_a" in extras:
         log("timing a Mode A denoising step")
-        rec["mode_a_step"] = mode_a_step(dev, sets[0]["w_vocab"], max(10, steps // 4))
+        rec["mode_a_step"] = mode_a_step(dev, sets[0]["w_vocab"], max(10, steps // 4), spin_s)
     del sets, base
     torch.cuda.empty_cache()
     if "single" in extras:
         log(f"{name}: timing the single-sequence step (batch 1)")
-        rec["single_sequence_step"] = single_sequence_step(dev, wl, max(20, steps // 2))
+        rec["single_sequence_step"] = single_sequence_step(dev, wl, max(20, steps // 2), spin_s)
     if want_cpu:
         log(f"{name}: timing the float64 CPU oracle (reference baseline)")
         rec["cpu_baseline"] = cpu_baseline(wl, x, c, sel)
@@ -308,6 +334,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--spin-up", type=float, default=SPIN_UP_S,
+                    help="seconds of untimed work before each measurement's warm-up steps (GPU clock settling)")
     ap.add_argument("--workload", default=HEADLINE, choices=["qwen0.6b", "qwen1.7b", "qwen4b"],
                     help="workload of the headline value")
     ap.add_argument("--only", action="store_true", help="time the headline workload only (no sub-workloads)")
@@ -341,12 +369,12 @@ def main():
         return set()
 
     head = measure_workload(args.workload, args.steps, args.warmup, extras_of(args.workload),
-                            not args.no_cpu_baseline)
+                            not args.no_cpu_baseline, args.spin_up)
     subs = {}
     if not args.only:
         for name in SUB_WORKLOADS + [HEADLINE]:
             if name != args.workload and name not in subs:
-                subs[name] = measure_workload(name, args.steps, args.warmup, extras_of(name), False)
+                subs[name] = measure_workload(name, args.steps, args.warmup, extras_of(name), False, args.spin_up)
 
     result = {
         "metric": METRIC,
@@ -355,6 +383,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "clock_spin_up_s": args.spin_up,
         "ms_per_step": head["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
@@ -378,11 +407,11 @@ def main():
     if subs:
         result["workloads"] = subs
     if not args.no_extras:
-        result["layout_attention"] = layout_attention(dev, max(5, args.steps // 10))
+        result["layout_attention"] = layout_attention(dev, max(5, args.steps // 10), args.spin_up)
     print(json.dumps(result), flush=True)
 
 
-def graph_step(step, sets, K):
+def graph_step(step, sets, K, spin_s):
     """The scoring step captured once per input copy in a HIP graph
     (torch.cuda.CUDAGraph over the library's launches) and replayed: the same
     kernels without the host-side launch path between them."""
@@ -402,6 +431,8 @@ def graph_step(step, sets, K):
         with torch.cuda.graph(g):
             step(s, Z.PASS_DIFFUSION)
         graphs.append(g)
+    ctr = itertools.count()
+    spin_up(lambda: graphs[next(ctr) % len(graphs)].replay(), spin_s)
     for g in graphs:
         g.replay()
     torch.cuda.synchronize()
@@ -415,7 +446,7 @@ def graph_step(step, sets, K):
     return {"step_us": us, "steps_per_s": 1e6 / us}
 
 
-def verification_step(dev, wl, s, conf_out, sel_out, K):
+def verification_step(dev, wl, s, conf_out, sel_out, K, spin_s):
     """The step after scoring (Sec. 5.2 "Verification phase", "KV cache
     update"): AR_INFILL attention of the draft tokens, confidence of the draft
     ids (the scoring step's argmax) as targets, acceptance of the selected
@@ -462,9 +493,13 @@ def verification_step(dev, wl, s, conf_out, sel_out, K):
         if evs:
             evs[4].record()
 
-    for _ in range(3):
+    def reset_and_run():
         plens.copy_(plens0)
         one()
+
+    spin_up(reset_and_run, spin_s)
+    for _ in range(3):
+        reset_and_run()
     torch.cuda.synchronize()
     # steps run back to back (the reset is a copy on the same stream, between
     # the timed events); the host reads the events and counts once at the end
@@ -485,7 +520,7 @@ def verification_step(dev, wl, s, conf_out, sel_out, K):
             "tokens_appended_per_row": statistics.mean(appended), "token_threshold": thr}
 
 
-def sampled_draft(dev, wl, sets, K, greedy_ms):
+def sampled_draft(dev, wl, sets, K, greedy_ms, spin_s):
     """Drafting with temperature (Sec. 5.2 "Sampling from categorical
     distribution"): the LM-head reduction with Gumbel-max sampling fused in,
     timed alone on the scoring step's hidden states, one Philox offset per
@@ -500,9 +535,16 @@ def sampled_draft(dev, wl, sets, K, greedy_ms):
     out["sample_id"] = torch.empty(M, dtype=torch.int32, device=dev)
     ws = torch.empty(_lib.slot_sample_workspace_size(_lib.ConfDesc(n_rows=M, hidden=H, vocab=V, dtype=1)),
                      dtype=torch.uint8, device=dev)
-    for i in range(3):
+    ctr = itertools.count()
+
+    def sample_once():
+        i = next(ctr)
         Z.slot_sample(sets[i % len(sets)]["hidden"], sets[i % len(sets)]["w_vocab"], 1.0, 2024, i, out=out,
                       workspace=ws)
+
+    spin_up(sample_once, spin_s)
+    for _ in range(3):
+        sample_once()
     torch.cuda.synchronize()
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
     for i in range(K):
@@ -516,7 +558,7 @@ def sampled_draft(dev, wl, sets, K, greedy_ms):
             "uniforms_per_s": M * V / (us * 1e-6), "vs_greedy_reduction": us / (greedy_ms * 1e3)}
 
 
-def mode_a_step(dev, w_vocab, K):
+def mode_a_step(dev, w_vocab, K, spin_s):
     """One denoising step of Mode A (Sec. 5.1) at the modeA workload: causal
     attention of the 4 tokens revealed at the previous step and the 256 masked
     ones after a 2048-token prompt, Gumbel-max sampling of the masked rows,
@@ -598,10 +640,16 @@ def mode_a_step(dev, w_vocab, K):
     result = {"workload": f"modeA: B={B} Hq/Hkv={Hq}/{Hkv} D={D} P={P} rows={R} ({k_prev} revealed + {Nt} masked) "
                           f"H={wl.hidden} V={wl.vocab}"}
     for rule, name in ((Z.REVEAL_CONFIDENCE, "confidence"), (Z.REVEAL_RANDOM, "random")):
-        for i in range(3):
+        ctr = itertools.count()
+
+        def reset_and_run():
             plens.copy_(plens0)
             mask.copy_(mask0)
-            one(i, rule)
+            one(next(ctr), rule)
+
+        spin_up(reset_and_run, spin_s)
+        for _ in range(3):
+            reset_and_run()
         torch.cuda.synchronize()
         ev_steps = []
         for i in range(K):  # back to back; the resets run between the timed events
@@ -643,7 +691,7 @@ def copy_calibration(dev, K):
                       "gbps": 2 * n / (ms * 1e-3) / 1e9}), flush=True)
 
 
-def single_sequence_step(dev, wl, K):
+def single_sequence_step(dev, wl, K, spin_s):
     """The scoring step of one sequence (batch 1 of the same model and slot
     shape): the latency a single request sees.  Its 64 draft rows take the
     reduction's 64-row tile.  Inputs rotate over three copies of W."""
@@ -680,6 +728,8 @@ def single_sequence_step(dev, wl, K):
         if evs:
             evs[3].record()
 
+    ctr = itertools.count()
+    spin_up(lambda: one(next(ctr)), spin_s)
     for i in range(5):
         one(i)
     torch.cuda.synchronize()
@@ -711,6 +761,8 @@ def single_sequence_step(dev, wl, K):
             one(i)
         graphs.append(g)
     torch.cuda.synchronize()
+    ctr = itertools.count()
+    spin_up(lambda: graphs[next(ctr) % 3].replay(), spin_s)
     for i in range(3):
         graphs[i].replay()
     torch.cuda.synchronize()
@@ -725,7 +777,7 @@ def single_sequence_step(dev, wl, K):
             "graph_step_us": us_graph, "graph_steps_per_s": 1e6 / us_graph}
 
 
-def layout_attention(dev, K):
+def layout_attention(dev, K, spin_s):
     """Causal attention over the reordered training layout (B=8, 16/8 heads,
     N=4096 = 128 slots x 32 tokens, every slot AR_INFILL with earlier slots
     visible), through zarya_slot_attn with cross_slot = CAUSAL and no prefix."""
@@ -742,6 +794,7 @@ def layout_attention(dev, K):
     out = torch.empty_like(xd["q"])
     run = lambda: Z.slot_attn(xd["q"], None, None, xd["k_slot"], xd["v_slot"], wl.n_slots, wl.slot_len,
                               pass_=Z.PASS_AR_INFILL, cross_slot=Z.CROSS_SLOT_CAUSAL, out=out, want_lse=False)
+    spin_up(run, spin_s)
     for _ in range(2):
         run()
     torch.cuda.synchronize()
