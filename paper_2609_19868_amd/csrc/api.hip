@@ -238,6 +238,13 @@ zarya_status run_conf(const zarya_conf_desc* d, const zarya_sample_params* sp, c
   p.part_idx = reinterpret_cast<int*>(ws + 2 * part);
   p.row_index = row_index;
   p.hidden_rows = hidden_rows;
+  if (d->dtype == ZARYA_DTYPE_BF16) {
+    // the row tiles present among one XCD's work items (a contiguous run of
+    // per_xcd items, row tile fastest) and the hidden rows they re-read
+    const int64_t br = conf_tile_rows(d->n_rows);
+    const int64_t rows_on_xcd = std::min<int64_t>(d->n_rows, std::min(pl.n_rt, p.per_xcd) * br);
+    p.w_stream = (size_t)rows_on_xcd * d->hidden * 2 <= kConfXResidentBytes ? 1 : 0;
+  }
   if (sp) {
     p.part_g = reinterpret_cast<float*>(ws + 3 * part);
     p.part_gi = reinterpret_cast<int*>(ws + 4 * part);

@@ -61,9 +61,12 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, 
 // no 64-bit address arithmetic per load.  Only voffset is checked against the
 // buffer's size (soffset is not): an access whose voffset is past the end
 // reads zeros, while one whose soffset carries it past the end is not caught.
+// AUX: cache-policy bits of the load (0: default; kLoadNonTemporal).
+constexpr int kLoadNonTemporal = 2;
+template <int AUX = 0>
 __device__ __forceinline__ void dmab16(__amdgpu_buffer_rsrc_t rsrc, void* lds_base, uint32_t voffset,
                                        uint32_t soffset) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_ptr)lds_base, 16, voffset, soffset, 0, 0);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_ptr)lds_base, 16, voffset, soffset, 0, AUX);
 }
 
 // Wait until at most N vector-memory operations of this wave are in flight

@@ -69,6 +69,9 @@ struct ConfParams {
   // merge marks out-of-range rows).
   const int32_t* row_index;
   int hidden_rows;
+  // bf16 path: W is loaded non-temporally (the hidden rows an XCD's work
+  // items re-read fit in its L2 beside the W stream; see kConfXResidentBytes)
+  int w_stream;
 };
 
 // Hidden row of output row r.
@@ -173,6 +176,14 @@ constexpr int kConfTargetWGs = 256;
 // every bf16 call up to 65536 rows (row tiles x vocabulary groups <= 256, 12
 // bytes per row and group).
 constexpr size_t kConfScratchBytes = (size_t)1 << 20;
+// Largest hidden-row footprint per XCD (rows of the row tiles among its work
+// items x H x 2 bytes) for which W is loaded non-temporally: up to this size
+// the hidden tiles, re-read once per vocab tile, stay in the 4 MB L2 instead
+// of being evicted by the W stream (measured on MI355X: at 2 MB the LM head's
+// L2-miss traffic falls from 1.61x to 1.11x its algorithmic bytes and the
+// kernel gains 2-4%; at 3 MB 1.15x and equal time; from 4 MB the hidden rows
+// no longer fit either way and non-temporal W costs traffic and 1% of time).
+constexpr size_t kConfXResidentBytes = (size_t)3 << 20;
 constexpr int conf_tile_rows(int n_rows) { return n_rows <= kConfSmallMaxRows ? kConfSmallBR : kConfBR; }
 
 hipError_t launch_slot_attn_bf16(const AttnParams& p, int head_dim, hipStream_t stream);

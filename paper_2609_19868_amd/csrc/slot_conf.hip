@@ -261,8 +261,10 @@ __device__ __forceinline__ void store_partials(const ConfParams& p, int vg, int 
 // BK: contraction depth per stage.  The W tile streams from HBM through a
 // ring of NSW LDS buffers (prefetch distance NSW - 1 stages), the hidden tile
 // (re-read for every vocab tile, so served from L2) through a ring of NSX.
-// Partials are written per (vocabulary group, row).
-template <int NW, int BR, int BK, int NSW, int NSX, bool SAMPLE>
+// W_NT: the W loads are non-temporal, so that the W stream does not evict the
+// hidden tiles from L2 (for launches whose hidden rows fit there).  Partials
+// are written per (vocabulary group, row).
+template <int NW, int BR, int BK, int NSW, int NSX, bool SAMPLE, bool W_NT>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4))) void slot_conf_bf16_kernel(
     ConfParams p) {
   constexpr int ATB = BV * BK * 2;    // bytes of the W tile of one stage
@@ -363,7 +365,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW / 4)
     uint8_t* dst = &lds_w[cw.slot][wave_u * 1024];
     const uint32_t off = (!k_ragged || kk + BK <= H) ? a_off : a_off + ragged_shift(kk);
 #pragma unroll
-    for (int j = 0; j < CPA; ++j) dmab16(rsrc_w, dst + NW * j * 1024, off + j * a_step, 2u * kk);
+    for (int j = 0; j < CPA; ++j) dmab16<W_NT ? kLoadNonTemporal : 0>(rsrc_w, dst + NW * j * 1024, off + j * a_step, 2u * kk);
     advance(cw, NSW);
   };
   auto issue_x = [&]() {  // the hidden tile of stage cx.st
@@ -669,22 +671,27 @@ __global__ __launch_bounds__(256) void slot_conf_merge_kernel(ConfMergeParams p)
   if (p.target_ids && p.target_prob) p.target_prob[row] = tgt_ok && !bad ? fast_exp2(zt * kLog2e - lse2) : nan;
 }
 
-hipError_t launch_slot_conf_bf16(const ConfParams& p, hipStream_t stream) {
+template <int NW, int BR, bool SAMPLE>
+void launch_conf_tile(const ConfParams& p, hipStream_t stream) {
   const dim3 grid(8 * p.per_xcd);
+  if (p.w_stream) {
+    slot_conf_bf16_kernel<NW, BR, kConfBK, kConfNSW, kConfNSX, SAMPLE, true><<<grid, dim3(NW * 64), 0, stream>>>(p);
+  } else {
+    slot_conf_bf16_kernel<NW, BR, kConfBK, kConfNSW, kConfNSX, SAMPLE, false><<<grid, dim3(NW * 64), 0, stream>>>(p);
+  }
+}
+
+hipError_t launch_slot_conf_bf16(const ConfParams& p, hipStream_t stream) {
   if (conf_tile_rows(p.M) == kConfSmallBR) {
     if (p.part_g) {
-      slot_conf_bf16_kernel<kConfSmallNW, kConfSmallBR, kConfBK, kConfNSW, kConfNSX, true>
-          <<<grid, dim3(kConfSmallNW * 64), 0, stream>>>(p);
+      launch_conf_tile<kConfSmallNW, kConfSmallBR, true>(p, stream);
     } else {
-      slot_conf_bf16_kernel<kConfSmallNW, kConfSmallBR, kConfBK, kConfNSW, kConfNSX, false>
-          <<<grid, dim3(kConfSmallNW * 64), 0, stream>>>(p);
+      launch_conf_tile<kConfSmallNW, kConfSmallBR, false>(p, stream);
     }
   } else if (p.part_g) {
-    slot_conf_bf16_kernel<kConfNW, kConfBR, kConfBK, kConfNSW, kConfNSX, true>
-        <<<grid, dim3(kConfNW * 64), 0, stream>>>(p);
+    launch_conf_tile<kConfNW, kConfBR, true>(p, stream);
   } else {
-    slot_conf_bf16_kernel<kConfNW, kConfBR, kConfBK, kConfNSW, kConfNSX, false>
-        <<<grid, dim3(kConfNW * 64), 0, stream>>>(p);
+    launch_conf_tile<kConfNW, kConfBR, false>(p, stream);
   }
   return hipGetLastError();
 }

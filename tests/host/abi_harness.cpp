@@ -75,9 +75,13 @@ static void check_conf(const ConfParams& p) {
   CHECK(p.row_index != nullptr || p.hidden_rows == p.M);
 }
 
+static ConfParams g_last_conf;  // the parameters of the last bf16 LM-head launch
+
 hipError_t launch_slot_conf_bf16(const ConfParams& p, hipStream_t) {
   ++g_launches;
+  g_last_conf = p;
   check_conf(p);
+  CHECK(p.w_stream == 0 || p.w_stream == 1);
   CHECK((int64_t)p.n_rt * conf_tile_rows(p.M) >= p.M);
   CHECK(p.n_vg <= (p.V + 31) / 32);
   return hipErrorNoDevice;
@@ -303,10 +307,45 @@ static void budget_cases(std::mt19937_64& rng) {
   }
 }
 
+// W is loaded non-temporally exactly when the hidden rows among one XCD's
+// work items (all of them for every shape here: each XCD holds whole vocab
+// groups) fit in 3 MB: the 0.6B-scale head (1024 x 1024: 2 MB) and single
+// sequences, not the 1.7B (2048 x 2048) or 4B (1024 x 2560) heads.
+static void conf_named_plans() {
+  struct Case {
+    int M, H, w_stream;
+  };
+  const Case cases[] = {{1024, 1024, 1}, {2048, 2048, 0}, {1024, 2560, 0}, {1024, 1536, 1}, {1024, 2048, 0},
+                        {64, 1024, 1},   {128, 2560, 1},  {2048, 1024, 0}};
+  for (const Case& c : cases) {
+    zarya_conf_desc d{};
+    d.n_rows = c.M;
+    d.hidden = c.H;
+    d.vocab = 151936;
+    d.dtype = ZARYA_DTYPE_BF16;
+    size_t ws = 0;
+    CHECK(zarya_slot_confidence_workspace_size(&d, &ws) == ZARYA_OK);
+    g_ws_lo = 0x100000000ull;
+    g_ws_hi = g_ws_lo + ws;
+    void* p = fake(0x200000000ull);
+    const int before = g_launches;
+    expect_launch(zarya_slot_confidence(&d, p, p, nullptr, (float*)p, (int32_t*)p, nullptr, nullptr, fake(g_ws_lo), ws,
+                                        nullptr),
+                  before, "conf named plan");
+    if (zarya::g_last_conf.w_stream != c.w_stream) {
+      std::printf("FAIL conf plan %d x %d: w_stream %d (expected %d)\n", c.M, c.H, zarya::g_last_conf.w_stream,
+                  c.w_stream);
+      ++g_fail;
+    }
+    ++g_checks;
+  }
+}
+
 int main() {
   std::mt19937_64 rng(20260);
   attn_cases(rng);
   named_plans();
+  conf_named_plans();
   conf_cases(rng);
   small_call_cases();
   budget_cases(rng);
