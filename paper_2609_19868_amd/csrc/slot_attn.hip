@@ -75,11 +75,26 @@ __global__ __launch_bounds__(NWAVE * 64) __attribute__((amdgpu_waves_per_eu(ZARY
   static_assert(CPW * NWAVE * 1024 == TILEB, "tile must split into 1 KB chunks per wave");
   __shared__ __attribute__((aligned(16))) uint8_t lds[NS][2][TILEB];
 
-  const int w = xcd_work_index(blockIdx.x, p.per_xcd, p.n_items);
-  if (w < 0) return;
-  const int rb = w % p.n_rb;
-  const int split = (w / p.n_rb) % p.n_split;
-  const int bg = w / (p.n_rb * p.n_split);  // b * Hkv + g
+  int rb, split, bg;  // row block, prefix split, b * Hkv + g
+  if (p.heavy_first) {
+    // Causal launch whose XCDs each hold whole GQA groups (one split, T a
+    // multiple of RB): an XCD walks its groups' row blocks heaviest first --
+    // the last token block of every head, then the one before -- so the
+    // longest work items start first and the short ones fill the tail.
+    const int x = blockIdx.x & 7, k = blockIdx.x >> 3;
+    const int gpx = p.per_xcd / p.n_rb;  // groups per XCD
+    const int rank = k / gpx;            // 0: heaviest
+    const int nbh = p.T / RB;            // row blocks per head
+    rb = (rank % p.G) * nbh + (nbh - 1 - rank / p.G);
+    split = 0;
+    bg = x * gpx + k % gpx;
+  } else {
+    const int w = xcd_work_index(blockIdx.x, p.per_xcd, p.n_items);
+    if (w < 0) return;
+    rb = w % p.n_rb;
+    split = (w / p.n_rb) % p.n_split;
+    bg = w / (p.n_rb * p.n_split);
+  }
   const int b = bg / p.Hkv;
   // this batch row's prefix length (rows differ after KV-cache appends)
   const int Pb = p.prefix_lens ? min(max(p.prefix_lens[b], 0), p.P) : p.P;

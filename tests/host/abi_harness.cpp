@@ -12,6 +12,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <random>
+#include <string>
 #include <vector>
 
 #include "kernels.hpp"
@@ -49,6 +50,9 @@ hipError_t launch_slot_attn_bf16(const AttnParams& p, int head_dim, hipStream_t)
   CHECK((int64_t)p.n_rb * p.rows_per_block >= p.R && (int64_t)(p.n_rb - 1) * p.rows_per_block < p.R &&
         p.R == p.G * p.T);
   CHECK(p.n_items == p.B * p.Hkv * p.n_split * p.n_rb);
+  // heavy-first dispatch only where every XCD holds whole groups of one split
+  CHECK(!p.heavy_first || (p.cross == 1 && p.n_split == 1 && p.T % p.rows_per_block == 0 && (p.B * p.Hkv) % 8 == 0 &&
+                           p.per_xcd * 8 == p.n_items && p.per_xcd % p.n_rb == 0 && p.n_rb * p.rows_per_block == p.R));
   CHECK(p.per_xcd * 8 >= p.n_items && (p.per_xcd - 1) * 8 < p.n_items);
   if (p.n_split > 1) {
     CHECK(in_ws(p.part_o, (size_t)p.n_split * p.rows_total * head_dim * 4));
@@ -213,6 +217,11 @@ static void named_plans() {
                                   nullptr),
                   before, c.name);
     const zarya::AttnParams& a = zarya::g_last_attn;
+    // the training layout (causal, 8 x 8 groups, T = 4096) dispatches heaviest first
+    if ((a.heavy_first != 0) != (std::string(c.name) == "layout")) {
+      std::printf("FAIL plan %s: heavy_first %d\n", c.name, a.heavy_first);
+      ++g_fail;
+    }
     if (a.rows_per_block != c.rows_per_block || a.n_rb != c.n_rb || a.n_split != c.n_split) {
       std::printf("FAIL plan %s: rows/block %d, row blocks %d, splits %d (expected %d, %d, %d)\n", c.name,
                   a.rows_per_block, a.n_rb, a.n_split, c.rows_per_block, c.n_rb, c.n_split);

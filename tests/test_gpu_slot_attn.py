@@ -93,6 +93,21 @@ def test_bf16_per_slot_pass_and_cross_causal():
         check_attn(to_f64(out), to_f64(lse), O, L, "bf16", f"slot_pass cross={cross}")
 
 
+def test_bf16_cross_causal_with_prefix_heavy_first():
+    """Cross-slot causal order after a prefix, one split, 8 GQA groups and
+    T = 256 (a multiple of the 128-row blocks): the launch that dispatches
+    row blocks heaviest first; both passes, every head against the oracle."""
+    dev = require_gpu()
+    wl = W.WORKLOADS["qwen0.6b"].replace(batch=2, n_q_heads=8, n_kv_heads=4, prefix_len=300, n_slots=16,
+                                         slot_len=16, hidden=0, vocab=0, seed=82)
+    xd, xf = attn_inputs_dev(wl, dev)
+    for pass_, pname in PASSES:
+        say(f"slot_attn cross causal heavy-first {pname}")
+        out, lse = _run(xd, wl, pass_, cross=Z.CROSS_SLOT_CAUSAL, splits=1)
+        O, L = _oracle(xf, wl, pass_, cross=oracle.CROSS_SLOT_CAUSAL)
+        check_attn(to_f64(out), to_f64(lse), O, L, "bf16", f"cross causal heavy-first {pname}")
+
+
 @pytest.mark.parametrize("over", [dict(), dict(n_q_heads=8, n_kv_heads=2)], ids=["rows128", "rows256_wide"])
 def test_bf16_split_counts_agree_and_runs_are_bitwise_identical(over):
     dev = require_gpu()
@@ -231,9 +246,13 @@ def _layout_case(wl, dev, variant):
 
 
 @pytest.mark.parametrize("variant", [False, True], ids=["causal", "masked_bidirectional"])
-def test_training_layout_small(variant):
+@pytest.mark.parametrize("shape", [dict(batch=2, n_q_heads=4, n_kv_heads=2, n_slots=16, slot_len=32),
+                                   # 8 GQA groups and T a multiple of 128 rows: the heaviest-first dispatch
+                                   dict(batch=2, n_q_heads=8, n_kv_heads=4, n_slots=8, slot_len=32)],
+                         ids=["four_groups", "eight_groups_heavy_first"])
+def test_training_layout_small(variant, shape):
     dev = require_gpu()
-    wl = W.WORKLOADS["layout"].replace(batch=2, n_q_heads=4, n_kv_heads=2, n_slots=16, slot_len=32, seed=81)
+    wl = W.WORKLOADS["layout"].replace(**shape, seed=81)
     _layout_case(wl, dev, variant)
 
 
