@@ -412,8 +412,7 @@ zarya_status zarya_slot_attn(const zarya_slot_attn_desc* d, const void* q, const
   // with a causal cross-slot order the row blocks' key ranges grow with
   // their tokens: dispatch the longest first where the grid allows it
   const int64_t n_bg = (int64_t)d->batch * d->n_kv_heads;
-  p.heavy_first = d->cross_slot == ZARYA_CROSS_SLOT_CAUSAL && pl.n_split == 1 && pl.T % pl.rows_per_block == 0 &&
-                  n_bg % 8 == 0;
+  p.heavy_first = d->cross_slot == ZARYA_CROSS_SLOT_CAUSAL && pl.n_split == 1 && n_bg % 8 == 0;
   return hip_status(launch_slot_attn_bf16(p, d->head_dim, stream), "slot_attn bf16 launch");
 }
 

@@ -27,8 +27,8 @@ struct AttnParams {
   int per_xcd, n_items;
   int rows_total;      // B * Hq * T
   int rows_per_block;  // kAttnRowsPerBlock or kAttnWideRowsPerBlock
-  // causal launch, one split, T % rows_per_block == 0, 8 | B*Hkv: every XCD
-  // holds B*Hkv/8 whole groups and takes their row blocks heaviest first
+  // causal launch, one split, 8 | B*Hkv: every XCD holds B*Hkv/8 whole
+  // groups and takes their row blocks heaviest first
   int heavy_first;
 };
 

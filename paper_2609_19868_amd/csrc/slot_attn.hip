@@ -8,7 +8,8 @@
 // cross_slot = CAUSAL.
 //
 // bf16 kernel design (one workgroup = 4 or 8 waves = up to 128 or 256 query
-// rows of one GQA group, i.e. G heads x T tokens flattened; one split of the
+// rows of one GQA group, i.e. G heads x T tokens flattened token-major, so a
+// block holds every head of a contiguous token range; one split of the
 // prefix keys):
 //  * K/V tiles of 64 keys are staged in LDS once and shared by every query
 //    row of the group (the prefix is read from HBM once per group and split).
@@ -77,15 +78,13 @@ __global__ __launch_bounds__(NWAVE * 64) __attribute__((amdgpu_waves_per_eu(ZARY
 
   int rb, split, bg;  // row block, prefix split, b * Hkv + g
   if (p.heavy_first) {
-    // Causal launch whose XCDs each hold whole GQA groups (one split, T a
-    // multiple of RB): an XCD walks its groups' row blocks heaviest first --
-    // the last token block of every head, then the one before -- so the
-    // longest work items start first and the short ones fill the tail.
+    // Causal launch whose XCDs each hold whole GQA groups (one split): an
+    // XCD walks its groups' row blocks heaviest first (the last tokens see
+    // the most keys), so the longest work items start first and the short
+    // ones fill the tail.
     const int x = blockIdx.x & 7, k = blockIdx.x >> 3;
     const int gpx = p.per_xcd / p.n_rb;  // groups per XCD
-    const int rank = k / gpx;            // 0: heaviest
-    const int nbh = p.T / RB;            // row blocks per head
-    rb = (rank % p.G) * nbh + (nbh - 1 - rank / p.G);
+    rb = p.n_rb - 1 - k / gpx;
     split = 0;
     bg = x * gpx + k % gpx;
   } else {
@@ -104,12 +103,17 @@ __global__ __launch_bounds__(NWAVE * 64) __attribute__((amdgpu_waves_per_eu(ZARY
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
   const int n = lane & 31, hh = lane >> 5;
 
-  // ---- this lane's query row and its visible range [vis_lo, vis_hi) of draft-token keys
-  const int row = rb * RB + wave * 32 + n;  // row of the GQA group, [0, G*T)
+  // ---- this lane's query row and its visible range [vis_lo, vis_hi) of
+  // draft-token keys.  A group's G*T rows are taken token-major (row = t*G +
+  // h), so a block's rows cover a contiguous token range of every head of
+  // the group and share one visible key range; mrow is the row's place in
+  // the head-major [G, T] layout of q and out.
+  const int row = rb * RB + wave * 32 + n;
   const bool row_ok = row < p.R;
+  const int mrow = (row % p.G) * p.T + row / p.G;
   int vis_lo = 0, vis_hi = 0;
   if (row_ok) {
-    const int t = row % p.T;
+    const int t = row / p.G;
     const int s = t / p.L, r = t - s * p.L;
     const int pass = p.slot_pass ? (int)p.slot_pass[b * p.S + s] : p.pass;
     const int own_lo = s * p.L;
@@ -124,14 +128,10 @@ __global__ __launch_bounds__(NWAVE * 64) __attribute__((amdgpu_waves_per_eu(ZARY
   const int n_pre = max(0, pre_end - pre_begin);
   int slot_lo = 0, n_slot = 0;
   if (split == p.n_split - 1) {
-    const int r0 = rb * RB;
-    const int r1 = min(p.R, r0 + RB) - 1;
-    int lo = 0, hi = p.T;
-    if (r0 / p.T == r1 / p.T) {  // rows of one head: tokens r0%T .. r1%T
-      const int t0 = r0 % p.T, t1 = r1 % p.T;
-      lo = p.cross ? 0 : (t0 / p.L) * p.L;
-      hi = min(p.T, (t1 / p.L + 1) * p.L);
-    }
+    const int t0 = rb * RB / p.G;                   // tokens of this block's rows
+    const int t1 = (min(p.R, rb * RB + RB) - 1) / p.G;
+    const int lo = p.cross ? 0 : (t0 / p.L) * p.L;
+    const int hi = min(p.T, (t1 / p.L + 1) * p.L);
     slot_lo = (lo / KT) * KT;
     n_slot = (hi - slot_lo + KT - 1) / KT;
   }
@@ -142,7 +142,7 @@ __global__ __launch_bounds__(NWAVE * 64) __attribute__((amdgpu_waves_per_eu(ZARY
   // pipeline's counted waits see only its own loads
   bf16x8 qf[NKS];
   {
-    const uint4* qrow = reinterpret_cast<const uint4*>(p.q + ((size_t)bg * p.R + (row_ok ? row : 0)) * D);
+    const uint4* qrow = reinterpret_cast<const uint4*>(p.q + ((size_t)bg * p.R + (row_ok ? mrow : 0)) * D);
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) {
       uint4 v = row_ok ? qrow[2 * ks + hh] : make_uint4(0, 0, 0, 0);
@@ -402,7 +402,7 @@ __global__ __launch_bounds__(NWAVE * 64) __attribute__((amdgpu_waves_per_eu(ZARY
   // ---- finalize: combine the two lane halves' partial sums
   const float l_tot = sum_xor32(l_run);
   if (!row_ok) return;
-  const size_t grow = (size_t)bg * p.R + row;  // row of the [B*Hq*T] output
+  const size_t grow = (size_t)bg * p.R + mrow;  // row of the [B*Hq*T] output
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
   const float lse2 = m_run * c2 + __log2f(l_tot);  // log2 units
   if (p.n_split == 1) {

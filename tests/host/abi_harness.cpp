@@ -51,8 +51,8 @@ hipError_t launch_slot_attn_bf16(const AttnParams& p, int head_dim, hipStream_t)
         p.R == p.G * p.T);
   CHECK(p.n_items == p.B * p.Hkv * p.n_split * p.n_rb);
   // heavy-first dispatch only where every XCD holds whole groups of one split
-  CHECK(!p.heavy_first || (p.cross == 1 && p.n_split == 1 && p.T % p.rows_per_block == 0 && (p.B * p.Hkv) % 8 == 0 &&
-                           p.per_xcd * 8 == p.n_items && p.per_xcd % p.n_rb == 0 && p.n_rb * p.rows_per_block == p.R));
+  CHECK(!p.heavy_first || (p.cross == 1 && p.n_split == 1 && (p.B * p.Hkv) % 8 == 0 && p.per_xcd * 8 == p.n_items &&
+                           p.per_xcd % p.n_rb == 0));
   CHECK(p.per_xcd * 8 >= p.n_items && (p.per_xcd - 1) * 8 < p.n_items);
   if (p.n_split > 1) {
     CHECK(in_ws(p.part_o, (size_t)p.n_split * p.rows_total * head_dim * 4));
@@ -217,8 +217,10 @@ static void named_plans() {
                                   nullptr),
                   before, c.name);
     const zarya::AttnParams& a = zarya::g_last_attn;
-    // the training layout (causal, 8 x 8 groups, T = 4096) dispatches heaviest first
-    if ((a.heavy_first != 0) != (std::string(c.name) == "layout")) {
+    // the causal launches over 8 x 8 groups (training layout) and 16 x 8
+    // (Mode A) dispatch heaviest first
+    const bool hf = std::string(c.name) == "layout" || std::string(c.name) == "modeA";
+    if ((a.heavy_first != 0) != hf) {
       std::printf("FAIL plan %s: heavy_first %d\n", c.name, a.heavy_first);
       ++g_fail;
     }

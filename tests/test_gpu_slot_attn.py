@@ -94,9 +94,9 @@ def test_bf16_per_slot_pass_and_cross_causal():
 
 
 def test_bf16_cross_causal_with_prefix_heavy_first():
-    """Cross-slot causal order after a prefix, one split, 8 GQA groups and
-    T = 256 (a multiple of the 128-row blocks): the launch that dispatches
-    row blocks heaviest first; both passes, every head against the oracle."""
+    """Cross-slot causal order after a prefix, one split and 8 GQA groups:
+    the launch that dispatches row blocks heaviest first; both passes, every
+    head against the oracle."""
     dev = require_gpu()
     wl = W.WORKLOADS["qwen0.6b"].replace(batch=2, n_q_heads=8, n_kv_heads=4, prefix_len=300, n_slots=16,
                                          slot_len=16, hidden=0, vocab=0, seed=82)
@@ -247,7 +247,7 @@ def _layout_case(wl, dev, variant):
 
 @pytest.mark.parametrize("variant", [False, True], ids=["causal", "masked_bidirectional"])
 @pytest.mark.parametrize("shape", [dict(batch=2, n_q_heads=4, n_kv_heads=2, n_slots=16, slot_len=32),
-                                   # 8 GQA groups and T a multiple of 128 rows: the heaviest-first dispatch
+                                   # 8 GQA groups, one split: the heaviest-first dispatch
                                    dict(batch=2, n_q_heads=8, n_kv_heads=4, n_slots=8, slot_len=32)],
                          ids=["four_groups", "eight_groups_heavy_first"])
 def test_training_layout_small(variant, shape):
