@@ -118,13 +118,12 @@ __device__ __forceinline__ void lds_wait() {
 __device__ __forceinline__ void lds_tie(bf16x8& x) { asm volatile("" : "+v"(x)); }
 __device__ __forceinline__ void lds_tie(v4i16& x) { asm volatile("" : "+v"(x)); }
 
-// max(a, b, c) in one v_max3_f32.  fmaxf() of values the compiler cannot
-// prove quiet (MFMA results, say) costs an extra canonicalising max per
-// operand; the operands here are finite.
+// max(a, b, c): the compiler folds the two maxima into one v_max3_f32.  It
+// must stay visible to the compiler (no inline assembly): the operands are
+// often MFMA results, which a VALU instruction may read only after the wait
+// states the compiler inserts for them.
 __device__ __forceinline__ float max3f(float a, float b, float c) {
-  float r;
-  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
-  return r;
+  return __builtin_fmaxf(__builtin_fmaxf(a, b), c);
 }
 
 // max(x, x of lane ^ 32) on every lane, through v_permlane32_swap (a VALU
