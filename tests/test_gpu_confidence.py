@@ -149,9 +149,14 @@ def test_bf16_ties_take_the_lowest_id():
     assert torch.all(res["argmax"] == 123), res["argmax"]
 
 
-def test_bf16_bitwise_deterministic():
+@pytest.mark.parametrize("rows,hidden", [(320, 512), (1024, 2560), (64, 1024)],
+                         ids=["nontemporal_w", "plain_w", "small_tile"])
+def test_bf16_bitwise_deterministic(rows, hidden):
+    """Two calls give identical bits: with W loaded non-temporally (the
+    hidden rows fit in L2), with plain W loads (1024 x 2560 rows do not), and
+    on the few-row tile."""
     dev = require_gpu()
-    wl = W.WORKLOADS["qwen0.6b"].replace(batch=1, n_slots=64, slot_len=5, hidden=512, vocab=20000, seed=92)
+    wl = W.WORKLOADS["qwen0.6b"].replace(batch=1, n_slots=rows, slot_len=1, hidden=hidden, vocab=20000, seed=92)
     c = W.confidence_inputs(wl)
     hd, wd = to_dev(c["hidden"], "bf16", dev), to_dev(c["w_vocab"], "bf16", dev)
     a = Z.slot_confidence(hd, wd)
