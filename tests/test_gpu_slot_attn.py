@@ -64,6 +64,8 @@ SMALL_BF16 = [
     ("wide_two_blocks", dict(batch=2, n_q_heads=8, n_kv_heads=2, prefix_len=333, n_slots=10, slot_len=10)),
     ("d64_wide", dict(batch=1, n_q_heads=8, n_kv_heads=2, head_dim=64, prefix_len=300, n_slots=8, slot_len=8)),
     ("g2_three_row_blocks", dict(batch=1, n_q_heads=4, n_kv_heads=2, prefix_len=190, n_slots=10, slot_len=13)),
+    # three query heads per KV head: the rows of a token are split across row blocks
+    ("g3_token_split", dict(batch=2, n_q_heads=6, n_kv_heads=2, prefix_len=200, n_slots=7, slot_len=11)),
 ]
 
 
@@ -93,13 +95,16 @@ def test_bf16_per_slot_pass_and_cross_causal():
         check_attn(to_f64(out), to_f64(lse), O, L, "bf16", f"slot_pass cross={cross}")
 
 
-def test_bf16_cross_causal_with_prefix_heavy_first():
+@pytest.mark.parametrize("over", [dict(n_q_heads=8, n_kv_heads=4), dict(n_q_heads=8, n_kv_heads=4, head_dim=64),
+                                  dict(n_q_heads=12, n_kv_heads=4)], ids=["g2", "g2_d64", "g3"])
+def test_bf16_cross_causal_with_prefix_heavy_first(over):
     """Cross-slot causal order after a prefix, one split and 8 GQA groups:
-    the launch that dispatches row blocks heaviest first; both passes, every
-    head against the oracle."""
+    the launch that dispatches row blocks heaviest first (D = 128 and 64;
+    three heads per group, whose token rows straddle row blocks); both
+    passes, every head against the oracle."""
     dev = require_gpu()
-    wl = W.WORKLOADS["qwen0.6b"].replace(batch=2, n_q_heads=8, n_kv_heads=4, prefix_len=300, n_slots=16,
-                                         slot_len=16, hidden=0, vocab=0, seed=82)
+    wl = W.WORKLOADS["qwen0.6b"].replace(batch=2, prefix_len=300, n_slots=16, slot_len=16, hidden=0, vocab=0,
+                                         seed=82, **over)
     xd, xf = attn_inputs_dev(wl, dev)
     for pass_, pname in PASSES:
         say(f"slot_attn cross causal heavy-first {pname}")
