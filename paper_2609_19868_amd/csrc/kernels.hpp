@@ -161,7 +161,7 @@ int64_t mask_budget_plan(int32_t n_masked, int32_t n_steps, double alpha0, uint6
 constexpr int kAppendMaxTokens = 8192;
 
 constexpr int kAttnKeysPerTile = 64;
-constexpr int kAttnF32RowsPerBlock = 64;    // float32 path: one query row per thread
+constexpr int kAttnF32RowsPerBlock = 32;    // float32 path: query rows per workgroup (D/16 lanes each)
 constexpr int kAttnRowsPerBlock = 128;      // four waves
 constexpr int kAttnWideRowsPerBlock = 256;  // eight waves: every K/V tile staged once for 256 rows
 // Tile configuration of the bf16 LM-head reduction (measured on MI355X over

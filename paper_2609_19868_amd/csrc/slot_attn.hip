@@ -491,39 +491,52 @@ __global__ __launch_bounds__(256) void slot_attn_merge_kernel(const float* __res
   if (lse && c == 0) lse[row] = (mx + __log2f(wsum)) * kLn2;
 }
 
-// float32 path: one thread per query row, plain FMA arithmetic, online softmax
-// with expf.  Serves small float32 problems and every mask variant.
+// float32 path: LPR = D/16 lanes per query row, each holding 16 elements of
+// the row's q and output; a score is the lanes' partial dot products summed
+// across the group (then taken from the group's first lane, so every lane
+// of a row follows the same online softmax, with expf).  Plain FMA
+// arithmetic; serves small float32 problems and every mask variant.
 template <int D>
-__global__ __launch_bounds__(kAttnF32RowsPerBlock) void slot_attn_f32_kernel(AttnParams32 p) {
-  const int gid = blockIdx.x * kAttnF32RowsPerBlock + threadIdx.x;
-  if (gid >= p.rows_total) return;
-  const int t = gid % p.T;
-  const int h = (gid / p.T) % p.Hq;
-  const int b = gid / (p.T * p.Hq);
+__global__ __launch_bounds__(kAttnF32RowsPerBlock * (D / 16)) void slot_attn_f32_kernel(AttnParams32 p) {
+  constexpr int LPR = D / 16;  // lanes per row
+  static_assert(LPR >= 1 && (LPR & (LPR - 1)) == 0 && 64 % LPR == 0, "a row's lanes are a power of two in a wave");
+  const int sub = threadIdx.x % LPR;  // this lane's 16-element slice of the row
+  const int gid = blockIdx.x * kAttnF32RowsPerBlock + threadIdx.x / LPR;
+  const bool row_ok = gid < p.rows_total;
+  // lanes past the last row follow a valid row (the shuffles need every lane
+  // of a group) and store nothing
+  const int grow = row_ok ? gid : p.rows_total - 1;
+  const int t = grow % p.T;
+  const int h = (grow / p.T) % p.Hq;
+  const int b = grow / (p.T * p.Hq);
   const int g = h / p.G;
   const int s = t / p.L, r = t - s * p.L;
   const int pass = p.slot_pass ? (int)p.slot_pass[b * p.S + s] : p.pass;
   const int vis_hi = s * p.L + (pass == 0 ? p.L : r + 1);
   const int vis_lo = p.cross ? 0 : s * p.L;
+  const int lead = (int)(threadIdx.x % 64) & ~(LPR - 1);  // the group's first lane in the wave
 
-  float qv[D], o[D];
-  const float* qrow = p.q + (size_t)gid * D;
+  float qv[16], o[16];
+  const float* qrow = p.q + (size_t)grow * D + sub * 16;
 #pragma unroll
-  for (int d = 0; d < D; ++d) {
+  for (int d = 0; d < 16; ++d) {
     qv[d] = qrow[d] * p.scale;
     o[d] = 0.f;
   }
   float m = -INFINITY, l = 0.f;
   auto visit = [&](const float* krow, const float* vrow) {
-    float sc = 0.f;
+    float part = 0.f;
 #pragma unroll
-    for (int d = 0; d < D; ++d) sc = fmaf(qv[d], krow[d], sc);
+    for (int d = 0; d < 16; ++d) part = fmaf(qv[d], krow[sub * 16 + d], part);
+#pragma unroll
+    for (int off = LPR / 2; off > 0; off >>= 1) part += __shfl_xor(part, off);
+    const float sc = __shfl(part, lead);
     const float m_new = fmaxf(m, sc);
     const float c = expf(m - m_new);
     const float e = expf(sc - m_new);
     l = l * c + e;
 #pragma unroll
-    for (int d = 0; d < D; ++d) o[d] = fmaf(e, vrow[d], o[d] * c);
+    for (int d = 0; d < 16; ++d) o[d] = fmaf(e, vrow[sub * 16 + d], o[d] * c);
     m = m_new;
   };
   const size_t cbase = ((size_t)b * p.Hkv + g) * p.C * D;
@@ -531,11 +544,12 @@ __global__ __launch_bounds__(kAttnF32RowsPerBlock) void slot_attn_f32_kernel(Att
   for (int j = 0; j < Pb; ++j) visit(p.k_cache + cbase + (size_t)j * D, p.v_cache + cbase + (size_t)j * D);
   const size_t sbase = ((size_t)b * p.Hkv + g) * p.T * D;
   for (int j = vis_lo; j < vis_hi; ++j) visit(p.k_slot + sbase + (size_t)j * D, p.v_slot + sbase + (size_t)j * D);
-  float* orow = p.out + (size_t)gid * D;
+  if (!row_ok) return;
+  float* orow = p.out + (size_t)gid * D + sub * 16;
   const float inv = 1.f / l;
 #pragma unroll
-  for (int d = 0; d < D; ++d) orow[d] = o[d] * inv;
-  if (p.lse) p.lse[gid] = m + logf(l);
+  for (int d = 0; d < 16; ++d) orow[d] = o[d] * inv;
+  if (p.lse && sub == 0) p.lse[gid] = m + logf(l);
 }
 
 // ------------------------------------------------------------------ launchers
@@ -573,9 +587,9 @@ hipError_t launch_slot_attn_bf16(const AttnParams& p, int head_dim, hipStream_t 
 hipError_t launch_slot_attn_f32(const AttnParams32& p, int head_dim, hipStream_t stream) {
   const int grid = (p.rows_total + kAttnF32RowsPerBlock - 1) / kAttnF32RowsPerBlock;
   if (head_dim == 128) {
-    hipLaunchKernelGGL(slot_attn_f32_kernel<128>, dim3(grid), dim3(kAttnF32RowsPerBlock), 0, stream, p);
+    hipLaunchKernelGGL(slot_attn_f32_kernel<128>, dim3(grid), dim3(kAttnF32RowsPerBlock * 8), 0, stream, p);
   } else {
-    hipLaunchKernelGGL(slot_attn_f32_kernel<64>, dim3(grid), dim3(kAttnF32RowsPerBlock), 0, stream, p);
+    hipLaunchKernelGGL(slot_attn_f32_kernel<64>, dim3(grid), dim3(kAttnF32RowsPerBlock * 4), 0, stream, p);
   }
   return hipGetLastError();
 }

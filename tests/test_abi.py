@@ -110,7 +110,7 @@ def test_slot_attn_plan_reports_the_decomposition():
         assert (_lib.slot_attn_workspace_size(d) > 0) == (plan["prefix_splits"] > 1)
     d = _lib.SlotAttnDesc(batch=1, n_q_heads=2, n_kv_heads=1, head_dim=64, prefix_len=64, kv_capacity=64,
                           n_slots=4, slot_len=4, softmax_scale=0.125, pass_=0, cross_slot=0, dtype=0)
-    assert _lib.slot_attn_plan(d) == {"prefix_splits": 1, "rows_per_workgroup": 64, "workgroups": 1, "kernels": 1}
+    assert _lib.slot_attn_plan(d) == {"prefix_splits": 1, "rows_per_workgroup": 32, "workgroups": 1, "kernels": 1}
     assert _lib.lib().zarya_slot_attn_plan(ctypes.byref(d), None) == _lib.ERR_INVALID_ARGUMENT
 
 
