@@ -40,6 +40,8 @@ CASES = [
     ("qwen0.6b rows", dict(batch=16, n_slots=8, slot_len=8, hidden=1024, vocab=151936)),
     ("smaller", dict(batch=1, n_slots=60, slot_len=5, hidden=256, vocab=5003)),
     ("few rows (64-row tile)", dict(batch=1, n_slots=9, slot_len=5, hidden=512, vocab=20011)),
+    # 1024 rows x 2560: the hidden rows do not fit in L2, W is loaded with plain loads
+    ("4B-scale rows", dict(batch=8, n_slots=8, slot_len=16, hidden=2560, vocab=30011)),
 ]
 
 
