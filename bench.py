@@ -239,20 +239,25 @@ def measure_workload(name, steps, warmup, extras, want_cpu, spin_s=SPIN_UP_S):
             evs[3].record()
 
     def timed(pass_, K, Wm):
+        """K steps timed as a whole (no events between the kernels, which
+        would add their own packets to the timed stream), then K more with
+        events around each kernel for the per-kernel breakdown."""
         ctr = itertools.count()
         spin_up(lambda: step(sets[next(ctr) % n_sets], pass_), spin_s)
         for i in range(Wm):
             step(sets[i % n_sets], pass_)
         torch.cuda.synchronize()
-        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
         t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
         t_start.record()
         for i in range(K):
-            step(sets[i % n_sets], pass_, evs[i])
+            step(sets[i % n_sets], pass_)
         t_end.record()
         torch.cuda.synchronize()
         total_ms = t_start.elapsed_time(t_end)
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+        for i in range(K):
+            step(sets[i % n_sets], pass_, evs[i])
+        torch.cuda.synchronize()
         per = [[e[j].elapsed_time(e[j + 1]) for j in range(3)] for e in evs]
         return total_ms / K, [statistics.mean(p[j] for p in per) for j in range(3)], \
             [statistics.median(p[j] for p in per) for j in range(3)], \
